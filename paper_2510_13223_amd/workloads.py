@@ -1,0 +1,356 @@
+"""Seeded synthetic inputs for split paged decode attention.
+
+This module only *draws* inputs; it contains none of the attention
+arithmetic, so both the fp64 oracle and the HIP path can be fed from it
+without sharing any of the method's code.
+
+What is generated (all host NumPy arrays; bf16 values are carried as their
+uint16 bit patterns because NumPy has no bfloat16):
+
+* ``q``            uint16 [B, Hq, D]                      bf16 query of the decode step
+* ``k_cache``      uint16 [num_blocks, Hkv, bs, D]         bf16 keys, token-major tile per (block, kv-head)
+* ``v_cache``      uint16 [num_blocks, Hkv, D, bs]         bf16 values, dim-major tile per (block, kv-head)
+* ``block_table``  int32  [B, max_blocks_per_seq]          logical block -> physical block, -1 when unused
+* ``seq_lens``     int32  [B]                              tokens in the cache, current token included
+* ``kv_begin``     int32  [n_parts, B]                     partition p of sequence b covers tokens
+* ``kv_end``       int32  [n_parts, B]                     [kv_begin[p, b], kv_end[p, b])
+
+The paged, block-level KV layout is the one the serving system builds on
+(block-level KV management, Related Work); the split of each sequence's
+blocks into a local partition and migrated partitions follows the
+attention-level migration of Sec. 4.1(2) read as a split along token blocks.
+
+Recipe (every draw comes from its own PCG64 stream keyed by
+``(seed, config id, stream id[, chunk])`` so the arrays do not depend on the
+number of threads used):
+
+* Q, K, V ~ N(0, 1) in float32, rounded to bf16 round-to-nearest-even.
+  ``tiny`` scales Q by 1/sqrt(128) before rounding; ``fine`` adds one
+  N(0, 4) bias vector per kv-head to every key before rounding.
+* Physical blocks: a pool of ceil(1.2 * sum_b n_b) blocks, assigned by one
+  random permutation in logical (sequence, block) order.  Blocks no sequence
+  uses, and the slots of a sequence's last block past ``seq_len``, hold a
+  quiet-NaN bf16 poison pattern, so any read outside the covered tokens shows
+  up as NaN.  Table entries past a sequence's last block are -1.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import math
+import os
+from concurrent.futures import ThreadPoolExecutor
+from typing import Callable, Dict, List, Optional, Tuple
+
+import numpy as np
+
+HEAD_DIM = 128
+BLOCK_SIZE = 16
+BF16_NAN = np.uint16(0x7FC0)
+
+# Stream ids for independent PCG64 streams.
+_S_LENS, _S_SPLIT, _S_PERM, _S_Q, _S_K, _S_V, _S_BIAS = range(7)
+
+_CHUNK_BLOCKS = 2048  # logical blocks per generation chunk
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit patterns, round-to-nearest-even; NaN stays a quiet NaN."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32)
+    rounded = ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)).astype(np.uint16)
+    nan = np.isnan(x)
+    if nan.any():
+        rounded[nan] = BF16_NAN
+    return rounded
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns -> float32 (exact widening)."""
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def _rng(seed: int, cfg_id: int, stream: int, chunk: int = -1) -> np.random.Generator:
+    key = [int(seed), int(cfg_id), int(stream)]
+    if chunk >= 0:
+        key.append(int(chunk))
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(key)))
+
+
+@dataclasses.dataclass
+class Workload:
+    name: str
+    seed: int
+    num_q_heads: int
+    num_kv_heads: int
+    q: np.ndarray
+    k_cache: np.ndarray
+    v_cache: np.ndarray
+    block_table: np.ndarray
+    seq_lens: np.ndarray
+    kv_begin: np.ndarray
+    kv_end: np.ndarray
+    max_range_tokens: int
+
+    @property
+    def batch(self) -> int:
+        return int(self.q.shape[0])
+
+    @property
+    def n_parts(self) -> int:
+        return int(self.kv_begin.shape[0])
+
+    @property
+    def num_blocks(self) -> int:
+        return int(self.k_cache.shape[0])
+
+    @property
+    def max_blocks_per_seq(self) -> int:
+        return int(self.block_table.shape[1])
+
+    @property
+    def group(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+    def kv_bytes(self, part: Optional[int] = None) -> int:
+        """Algorithmic K+V bytes the covered tokens occupy (each read once)."""
+        per_tok = self.num_kv_heads * HEAD_DIM * 2 * 2
+        if part is None:
+            toks = int(np.sum(self.kv_end.astype(np.int64) - self.kv_begin))
+        else:
+            toks = int(np.sum(self.kv_end[part].astype(np.int64) - self.kv_begin[part]))
+        return toks * per_tok
+
+
+# ---------------------------------------------------------------------------
+# Sequence lengths and partition ranges for the five serving-shaped workloads
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class Config:
+    cfg_id: int
+    name: str
+    batch: int
+    num_q_heads: int
+    num_kv_heads: int
+    max_seq_len: int  # table width = max_seq_len / 16
+    q_scale: float = 1.0
+    key_bias_std: float = 0.0
+
+
+CONFIGS: Dict[str, Config] = {
+    "tiny": Config(1, "tiny", 4, 8, 2, 1024, q_scale=1.0 / math.sqrt(128.0)),
+    "llama3_8b": Config(2, "llama3_8b", 64, 32, 8, 4096),
+    "long": Config(3, "long", 8, 32, 8, 131072),
+    "mixed": Config(4, "mixed", 256, 32, 8, 16384),
+    "fine": Config(5, "fine", 512, 64, 8, 2048, key_bias_std=2.0),
+}
+
+
+def _nblk(L: int) -> int:
+    return (L + BLOCK_SIZE - 1) // BLOCK_SIZE
+
+
+def _split_at_block(L: int, j: int) -> List[Tuple[int, int]]:
+    cut = j * BLOCK_SIZE
+    return [(0, cut), (cut, L)]
+
+
+def _lens_and_ranges(cfg: Config, seed: int) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    rl = _rng(seed, cfg.cfg_id, _S_LENS)
+    rs = _rng(seed, cfg.cfg_id, _S_SPLIT)
+    B = cfg.batch
+    if cfg.name == "tiny":
+        lens = rl.integers(256, 1024, size=B, endpoint=True)
+        parts = []
+        for L in lens:
+            nb = _nblk(int(L))
+            j = int(rs.integers(1, nb - 1, endpoint=True))
+            parts.append(_split_at_block(int(L), j))
+    elif cfg.name == "llama3_8b":
+        lens = np.full(B, 4096)
+        nb = 256
+        migrated = int(round(0.3 * nb))
+        parts = [_split_at_block(4096, nb - migrated) for _ in range(B)]
+    elif cfg.name == "long":
+        lens = rl.integers(32768, 131072, size=B, endpoint=True)
+        parts = []
+        for L in lens:
+            nb = _nblk(int(L))
+            w = rs.dirichlet(np.ones(4)) * nb
+            sizes = np.floor(w).astype(np.int64)
+            rem = nb - int(sizes.sum())
+            order = np.argsort(-(w - sizes), kind="stable")
+            sizes[order[:rem]] += 1
+            cum = np.concatenate([[0], np.cumsum(sizes)])
+            parts.append([(int(min(cum[p] * BLOCK_SIZE, L)), int(min(cum[p + 1] * BLOCK_SIZE, L))) for p in range(4)])
+    elif cfg.name == "mixed":
+        z = rl.standard_normal(B)
+        lens = np.clip(np.rint(np.exp(math.log(1024.0) + z)), 16, 16384).astype(np.int64)
+        parts = []
+        for L in lens:
+            L = int(L)
+            if L > 2048:
+                nb = _nblk(L)
+                j = int(rs.integers(1, nb - 1, endpoint=True))
+                parts.append(_split_at_block(L, j))
+            else:
+                parts.append([(0, L), (L, L)])
+    elif cfg.name == "fine":
+        lens = np.full(B, 2048)
+        step = 128
+        parts = [[(p * step, (p + 1) * step) for p in range(16)] for _ in range(B)]
+    else:  # pragma: no cover
+        raise KeyError(cfg.name)
+    lens = np.asarray(lens, dtype=np.int32)
+    n_parts = len(parts[0])
+    begin = np.array([[parts[b][p][0] for b in range(B)] for p in range(n_parts)], dtype=np.int32)
+    end = np.array([[parts[b][p][1] for b in range(B)] for p in range(n_parts)], dtype=np.int32)
+    return lens, begin, end
+
+
+# ---------------------------------------------------------------------------
+# Pool / table / tensor generation
+# ---------------------------------------------------------------------------
+
+def _gen_normal_bf16(seed, cfg_id, stream, chunk, shape, scale=1.0, bias=None):
+    g = _rng(seed, cfg_id, stream, chunk)
+    x = g.standard_normal(size=shape, dtype=np.float32)
+    if scale != 1.0:
+        x *= np.float32(scale)
+    if bias is not None:
+        x += bias
+    return f32_to_bf16_bits(x)
+
+
+def build_workload(
+    name: str,
+    seed: int,
+    batch: int,
+    num_q_heads: int,
+    num_kv_heads: int,
+    seq_lens: np.ndarray,
+    kv_begin: np.ndarray,
+    kv_end: np.ndarray,
+    max_blocks_per_seq: int,
+    cfg_id: int = 99,
+    q_scale: float = 1.0,
+    key_bias_std: float = 0.0,
+    pool_factor: float = 1.2,
+    threads: Optional[int] = None,
+    kv_fill: Optional[Callable[[int, np.ndarray], None]] = None,
+) -> Workload:
+    """Draw Q, the paged K/V pools and the block table for given lengths and ranges."""
+    B, Hq, Hkv, D, bs = batch, num_q_heads, num_kv_heads, HEAD_DIM, BLOCK_SIZE
+    seq_lens = np.asarray(seq_lens, dtype=np.int32)
+    nbs = np.array([_nblk(int(L)) for L in seq_lens], dtype=np.int64)
+    if np.any(nbs > max_blocks_per_seq):
+        raise ValueError("sequence longer than the block table")
+    n_used = int(nbs.sum())
+    num_blocks = max(1, int(math.ceil(pool_factor * n_used)))
+
+    perm = _rng(seed, cfg_id, _S_PERM).permutation(num_blocks).astype(np.int64)
+    phys_of_logical = perm[:n_used]  # logical block i (in (b, j) order) -> physical block
+
+    table = np.full((B, max_blocks_per_seq), -1, dtype=np.int32)
+    owner_seq = np.empty(n_used, dtype=np.int64)
+    owner_blk = np.empty(n_used, dtype=np.int64)
+    pos = 0
+    for b in range(B):
+        nb = int(nbs[b])
+        table[b, :nb] = phys_of_logical[pos:pos + nb]
+        owner_seq[pos:pos + nb] = b
+        owner_blk[pos:pos + nb] = np.arange(nb)
+        pos += nb
+
+    bias = None
+    if key_bias_std:
+        bias = (_rng(seed, cfg_id, _S_BIAS).standard_normal((Hkv, D), dtype=np.float32) * np.float32(key_bias_std))
+
+    q = _gen_normal_bf16(seed, cfg_id, _S_Q, -1, (B, Hq, D), scale=q_scale)
+
+    k_cache = np.empty((num_blocks, Hkv, bs, D), dtype=np.uint16)
+    v_cache = np.empty((num_blocks, Hkv, D, bs), dtype=np.uint16)
+    used = np.zeros(num_blocks, dtype=bool)
+    used[phys_of_logical] = True
+    k_cache[~used] = BF16_NAN
+    v_cache[~used] = BF16_NAN
+
+    n_chunks = (n_used + _CHUNK_BLOCKS - 1) // _CHUNK_BLOCKS
+
+    def do_chunk(c: int) -> None:
+        lo, hi = c * _CHUNK_BLOCKS, min(n_used, (c + 1) * _CHUNK_BLOCKS)
+        n = hi - lo
+        kb = None if bias is None else bias[None, :, None, :]
+        kk = _gen_normal_bf16(seed, cfg_id, _S_K, c, (n, Hkv, bs, D), bias=kb)
+        vv = _gen_normal_bf16(seed, cfg_id, _S_V, c, (n, Hkv, bs, D))
+        # Poison the slots past seq_len in each sequence's last block.
+        last_len = seq_lens[owner_seq[lo:hi]] - owner_blk[lo:hi] * bs
+        tail = np.arange(bs)[None, :] >= last_len[:, None]  # [n, bs]
+        if tail.any():
+            kk.transpose(0, 2, 1, 3)[tail] = BF16_NAN
+            vv.transpose(0, 2, 1, 3)[tail] = BF16_NAN
+        phys = phys_of_logical[lo:hi]
+        k_cache[phys] = kk
+        v_cache[phys] = vv.transpose(0, 1, 3, 2)
+
+    nthr = threads or min(16, os.cpu_count() or 1)
+    if n_chunks > 1 and nthr > 1:
+        with ThreadPoolExecutor(max_workers=nthr) as ex:
+            list(ex.map(do_chunk, range(n_chunks)))
+    else:
+        for c in range(n_chunks):
+            do_chunk(c)
+
+    kv_begin = np.asarray(kv_begin, dtype=np.int32)
+    kv_end = np.asarray(kv_end, dtype=np.int32)
+    max_range = int(np.max(kv_end.astype(np.int64) - kv_begin)) if kv_begin.size else 0
+    return Workload(name, seed, Hq, Hkv, q, k_cache, v_cache, table, seq_lens, kv_begin, kv_end, max_range)
+
+
+def make_config(name: str, seed: int = 0, threads: Optional[int] = None) -> Workload:
+    """One of the five serving-shaped workloads: tiny, llama3_8b, long, mixed, fine."""
+    cfg = CONFIGS[name]
+    lens, begin, end = _lens_and_ranges(cfg, seed)
+    return build_workload(
+        cfg.name, seed, cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, lens, begin, end,
+        cfg.max_seq_len // BLOCK_SIZE, cfg_id=cfg.cfg_id, q_scale=cfg.q_scale,
+        key_bias_std=cfg.key_bias_std, threads=threads)
+
+
+def make_custom(
+    seed: int,
+    batch: int,
+    num_q_heads: int,
+    num_kv_heads: int,
+    seq_lens,
+    ranges,
+    max_blocks_per_seq: Optional[int] = None,
+    q_scale: float = 1.0,
+    key_bias_std: float = 0.0,
+    pool_factor: float = 1.2,
+) -> Workload:
+    """Small hand-shaped workload. ``ranges[p][b] = (begin, end)``."""
+    seq_lens = np.asarray(seq_lens, dtype=np.int32)
+    mb = max_blocks_per_seq or max(1, max(_nblk(int(L)) for L in seq_lens))
+    begin = np.array([[r[0] for r in part] for part in ranges], dtype=np.int32)
+    end = np.array([[r[1] for r in part] for part in ranges], dtype=np.int32)
+    return build_workload("custom", seed, batch, num_q_heads, num_kv_heads, seq_lens, begin, end, mb,
+                          cfg_id=100, q_scale=q_scale, key_bias_std=key_bias_std, pool_factor=pool_factor)
+
+
+def permute_physical(w: Workload, seed: int) -> Workload:
+    """Same logical content under a different physical block placement."""
+    g = _rng(seed, 1000, _S_PERM)
+    perm = g.permutation(w.num_blocks)  # old physical p -> new physical perm[p]
+    k2 = np.empty_like(w.k_cache)
+    v2 = np.empty_like(w.v_cache)
+    k2[perm] = w.k_cache
+    v2[perm] = w.v_cache
+    t2 = np.where(w.block_table >= 0, perm[np.maximum(w.block_table, 0)], -1).astype(np.int32)
+    return dataclasses.replace(w, k_cache=k2, v_cache=v2, block_table=t2)
+
+
+def unsplit_ranges(w: Workload) -> Tuple[np.ndarray, np.ndarray]:
+    """The single partition [0, seq_len) per sequence."""
+    return np.zeros((1, w.batch), dtype=np.int32), w.seq_lens[None, :].astype(np.int32).copy()

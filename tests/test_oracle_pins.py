@@ -1,0 +1,339 @@
+"""Pins of the fp64 oracle against facts fixed by the paper and by mathematics.
+
+None of these re-types the oracle's own formula: each compares it with an
+independent route (brute force, a library routine, closed forms of special
+inputs, invariants of the log-sum-exp merge, the paper's worked example).
+"""
+
+import hashlib
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import brute
+from paper_2510_13223_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _f64(bits):
+    return W.bf16_bits_to_f32(bits).astype(np.float64)
+
+
+def _small(seed=0, B=2, Hq=4, Hkv=2, lens=(37, 64), ranges=None, q_scale=1.0 / math.sqrt(128)):
+    lens = list(lens)
+    if ranges is None:
+        ranges = [[(0, min(16, L)) for L in lens], [(min(16, L), L) for L in lens]]
+    return W.make_custom(seed, B, Hq, Hkv, lens, ranges, q_scale=q_scale)
+
+
+def _set_k_row(w, b, g, t, values_bits):
+    blk = w.block_table[b, t // 16]
+    w.k_cache[blk, g, t % 16, :] = values_bits
+
+
+def _v_row(w, b, g, t):
+    blk = w.block_table[b, t // 16]
+    return _f64(w.v_cache[blk, g, :, t % 16])
+
+
+def _k_row(w, b, g, t):
+    blk = w.block_table[b, t // 16]
+    return _f64(w.k_cache[blk, g, t % 16, :])
+
+
+# --------------------------------------------------------------------------- inputs
+
+def test_bf16_rne_matches_torch():
+    rng = np.random.default_rng(5)
+    x = np.concatenate([
+        rng.standard_normal(100000).astype(np.float32),
+        (rng.standard_normal(1000) * 1e30).astype(np.float32),
+        (rng.standard_normal(1000) * 1e-39).astype(np.float32),  # subnormals
+        np.array([0.0, -0.0, np.inf, -np.inf, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, 3.3895314e38], np.float32),
+    ])
+    ours = W.f32_to_bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(ours, ref)
+
+
+def test_generator_deterministic_and_seeded():
+    a = W.make_config("tiny", 0)
+    b = W.make_config("tiny", 0)
+    c = W.make_config("tiny", 1)
+    for name in ("q", "k_cache", "v_cache", "block_table", "seq_lens", "kv_begin", "kv_end"):
+        ha = hashlib.sha256(getattr(a, name).tobytes()).hexdigest()
+        hb = hashlib.sha256(getattr(b, name).tobytes()).hexdigest()
+        assert ha == hb, name
+    assert hashlib.sha256(a.k_cache.tobytes()).hexdigest() != hashlib.sha256(c.k_cache.tobytes()).hexdigest()
+    # generation does not depend on the thread count
+    d = W.make_config("tiny", 0, threads=1)
+    np.testing.assert_array_equal(a.k_cache, d.k_cache)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_generator_poison_and_coverage(seed):
+    w = W.make_config("tiny", seed)
+    k = W.bf16_bits_to_f32(w.k_cache)
+    used = np.zeros(w.num_blocks, bool)
+    for b in range(w.batch):
+        L = int(w.seq_lens[b])
+        nb = (L + 15) // 16
+        assert np.all(w.block_table[b, nb:] == -1)
+        for j in range(nb):
+            blk = w.block_table[b, j]
+            assert not used[blk], "physical block used twice"
+            used[blk] = True
+            valid = min(16, L - 16 * j)
+            assert np.all(np.isfinite(k[blk, :, :valid, :]))
+            assert np.all(np.isnan(k[blk, :, valid:, :]))
+        # partitions tile [0, L) in order
+        assert w.kv_begin[0, b] == 0 and w.kv_end[-1, b] == L
+        assert np.all(w.kv_end[:-1, b] == w.kv_begin[1:, b])
+    assert np.all(np.isnan(k[~used]))
+    assert w.num_blocks == math.ceil(1.2 * used.sum())
+
+
+def test_paper_worked_example_kv_bytes():
+    """Sec. 4.2 worked example: 4096 B per token per layer, 128 KiB over 32 layers."""
+    g = json.load(open(os.path.join(GOLDEN, "kv_bytes_llama31_8b.json")))
+    assert g["d_model"] // g["h_total"] == g["d_head"]
+    w = W.make_custom(0, 1, g["h_total"], g["h_kv"], [16], [[(0, 16)]])
+    per_token = w.kv_bytes() // 16
+    assert per_token == g["s_kv_bytes_per_token_per_layer"]
+    assert per_token * g["layers"] == g["s_kv_total_bytes_per_token"]
+
+
+# --------------------------------------------------------------------------- oracle vs brute force / library
+
+def test_oracle_matches_brute_force():
+    w = _small(seed=3, lens=(37, 64), ranges=[[(0, 16), (5, 29)], [(16, 37), (29, 64)]])
+    for p in range(w.n_parts):
+        out, lse = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.kv_begin[p], w.kv_end[p])
+        for b in range(w.batch):
+            for h in range(4):
+                bo, bl = brute.attention(w.q.tolist(), w.k_cache.tolist(), w.v_cache.tolist(), w.block_table.tolist(),
+                                         w.seq_lens.tolist(), [(int(w.kv_begin[p, b]), int(w.kv_end[p, b]))], b, h, 2)
+                np.testing.assert_allclose(out[b, h], bo, rtol=0, atol=1e-13)
+                assert abs(lse[b, h] - bl) < 1e-13
+    # the merge equals brute force over the union, carrying l across partitions as l^(2) = l^(1) + sum A^(2)
+    outs, lses = oracle.workload_partials(w)
+    mo, ml = oracle.merge(outs, lses)
+    for b in range(w.batch):
+        for h in range(4):
+            rr = [(int(w.kv_begin[p, b]), int(w.kv_end[p, b])) for p in range(w.n_parts)]
+            bo, bl = brute.attention(w.q.tolist(), w.k_cache.tolist(), w.v_cache.tolist(), w.block_table.tolist(),
+                                     w.seq_lens.tolist(), rr, b, h, 2)
+            np.testing.assert_allclose(mo[b, h], bo, rtol=0, atol=1e-13)
+            assert abs(ml[b, h] - bl) < 1e-13
+
+
+def _dense_kv(w, b, g):
+    """Gather sequence b's K/V for kv head g into dense [L, D] arrays via NumPy fancy indexing."""
+    L = int(w.seq_lens[b])
+    t = np.arange(L)
+    blk = w.block_table[b, t // 16]
+    k = _f64(w.k_cache[blk, g, t % 16, :])
+    v = _f64(w.v_cache[blk, g, :, t % 16])  # advanced indices first -> [L, D]
+    return k, v
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_oracle_unsplit_matches_torch_sdpa(seed):
+    w = W.make_config("tiny", seed)
+    out, lse = oracle.workload_unsplit(w)
+    G = w.group
+    for b in range(w.batch):
+        for g in range(w.num_kv_heads):
+            k, v = _dense_kv(w, b, g)
+            qg = torch.from_numpy(_f64(w.q[b, g * G:(g + 1) * G]))[None, :, None, :]  # [1, G, 1, D]
+            kt = torch.from_numpy(k)[None, None].expand(1, G, -1, -1)
+            vt = torch.from_numpy(v)[None, None].expand(1, G, -1, -1)
+            ref = torch.nn.functional.scaled_dot_product_attention(qg, kt, vt, scale=1.0)[0, :, 0, :].numpy()
+            np.testing.assert_allclose(out[b, g * G:(g + 1) * G], ref, rtol=0, atol=1e-12)
+            ref_lse = torch.logsumexp(torch.from_numpy(k) @ qg[0, :, 0, :].T, dim=0).numpy()
+            np.testing.assert_allclose(lse[b, g * G:(g + 1) * G], ref_lse, rtol=0, atol=1e-12)
+
+
+# --------------------------------------------------------------------------- merge invariants
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_merge_of_any_split_equals_unsplit(seed):
+    w = W.make_config("tiny", seed)
+    uo, ul = oracle.workload_unsplit(w)
+    outs, lses = oracle.workload_partials(w)
+    mo, ml = oracle.merge(outs, lses)
+    np.testing.assert_allclose(mo, uo, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(ml, ul, rtol=0, atol=1e-12)
+    # a finer, non-block-aligned split into 5 pieces, one of them empty
+    rng = np.random.default_rng(seed)
+    begins, ends = [], []
+    for b in range(w.batch):
+        L = int(w.seq_lens[b])
+        cuts = np.sort(rng.integers(0, L, size=3))
+        edges = [0, int(cuts[0]), int(cuts[0]), int(cuts[1]), int(cuts[2]), L]
+        begins.append(edges[:-1])
+        ends.append(edges[1:])
+    begins = np.array(begins, np.int32).T
+    ends = np.array(ends, np.int32).T
+    po, pl = [], []
+    for p in range(begins.shape[0]):
+        o, l = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, begins[p], ends[p])
+        po.append(o)
+        pl.append(l)
+    assert np.any(np.isneginf(np.stack(pl)))
+    mo2, ml2 = oracle.merge(np.stack(po), np.stack(pl))
+    np.testing.assert_allclose(mo2, uo, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(ml2, ul, rtol=0, atol=1e-12)
+
+
+def test_merge_order_and_empty_parts():
+    w = W.make_config("tiny", 4)
+    outs, lses = oracle.workload_partials(w)
+    mo, ml = oracle.merge(outs, lses)
+    ro, rl = oracle.merge(outs[::-1].copy(), lses[::-1].copy())
+    np.testing.assert_allclose(ro, mo, rtol=0, atol=1e-14)
+    np.testing.assert_allclose(rl, ml, rtol=0, atol=1e-14)
+    junk = np.full_like(outs[:1], 12345.0)  # contents of an empty part are never read
+    eo = np.concatenate([junk, outs[:1], junk, outs[1:]])
+    el = np.concatenate([np.full_like(lses[:1], -np.inf), lses[:1], np.full_like(lses[:1], -np.inf), lses[1:]])
+    xo, xl = oracle.merge(eo, el)
+    np.testing.assert_array_equal(xo, mo)
+    np.testing.assert_array_equal(xl, ml)
+
+
+def test_empty_partition_and_all_empty_merge():
+    w = _small(seed=1, ranges=[[(7, 7), (0, 0)], [(7, 30), (0, 64)]])
+    o, l = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.kv_begin[0], w.kv_end[0])
+    assert np.all(o == 0.0) and np.all(np.isneginf(l))
+    mo, ml = oracle.merge(o[None], l[None])
+    assert np.all(mo == 0.0) and np.all(np.isneginf(ml))
+
+
+# --------------------------------------------------------------------------- closed forms of special inputs
+
+def test_single_key_returns_its_value_row():
+    w = _small(seed=2, lens=(50, 64), ranges=[[(17, 18), (63, 64)]])
+    out, lse = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.kv_begin[0], w.kv_end[0])
+    for b, t in ((0, 17), (1, 63)):
+        for h in range(4):
+            g = h // 2
+            np.testing.assert_array_equal(out[b, h], _v_row(w, b, g, t))
+            s = math.fsum((_f64(w.q[b, h]) * _k_row(w, b, g, t)).tolist())  # bf16 products are exact in fp64
+            assert lse[b, h] == s
+
+
+def test_equal_keys_give_mean_value():
+    w = _small(seed=3, lens=(64, 40), ranges=[[(3, 61), (0, 40)]])
+    for b in range(2):
+        for g in range(2):
+            row = w.k_cache[w.block_table[b, 0], g, 0, :].copy()
+            for t in range(int(w.kv_begin[0, b]), int(w.kv_end[0, b])):
+                _set_k_row(w, b, g, t, row)
+    out, lse = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.kv_begin[0], w.kv_end[0])
+    for b in range(2):
+        t0, t1 = int(w.kv_begin[0, b]), int(w.kv_end[0, b])
+        for h in range(4):
+            g = h // 2
+            vs = np.stack([_v_row(w, b, g, t) for t in range(t0, t1)])
+            mean = np.array([math.fsum(vs[:, d].tolist()) for d in range(128)]) / (t1 - t0)
+            np.testing.assert_allclose(out[b, h], mean, rtol=0, atol=1e-14)
+            s = math.fsum((_f64(w.q[b, h]) * _k_row(w, b, g, t0)).tolist())
+            assert abs(lse[b, h] - (s + math.log(t1 - t0))) < 1e-13
+
+
+def test_zero_keys_pin_coverage_counts():
+    w = W.make_config("tiny", 5)
+    w.k_cache[np.isfinite(W.bf16_bits_to_f32(w.k_cache))] = 0
+    outs, lses = oracle.workload_partials(w)
+    n = (w.kv_end - w.kv_begin).astype(np.float64)  # [P, B]
+    np.testing.assert_allclose(lses, np.log(n)[:, :, None].repeat(w.num_q_heads, 2), rtol=0, atol=1e-14)
+    assert np.all(np.rint(np.exp(lses)) == n[:, :, None])
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_dominant_key_pins_addressing(seed):
+    """A key along q whose score beats all others by > 110 makes out equal its V row."""
+    w = W.make_config("tiny", seed)
+    rng = np.random.default_rng(100 + seed)
+    G = w.group
+    for b in range(w.batch):
+        for g in range(w.num_kv_heads):
+            t0, t1 = int(w.kv_begin[1, b]), int(w.kv_end[1, b])
+            t = int(rng.integers(t0, t1))
+            qg = W.bf16_bits_to_f32(w.q[b, g * G]).astype(np.float32)
+            _set_k_row(w, b, g, t, W.f32_to_bf16_bits(qg * np.float32(300.0 / float(qg @ qg))))
+    out, lse = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.kv_begin[1], w.kv_end[1])
+    rng = np.random.default_rng(100 + seed)
+    for b in range(w.batch):
+        for g in range(w.num_kv_heads):
+            t = int(rng.integers(int(w.kv_begin[1, b]), int(w.kv_end[1, b])))
+            h = g * G  # the head the key was aimed at
+            np.testing.assert_allclose(out[b, h], _v_row(w, b, g, t), rtol=0, atol=1e-30)
+
+
+def test_physical_permutation_is_bit_identical():
+    w = W.make_config("tiny", 6)
+    w2 = W.permute_physical(w, 1)
+    assert not np.array_equal(w.block_table, w2.block_table)
+    a = oracle.workload_partials(w)
+    b = oracle.workload_partials(w2)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+
+
+def test_key_bias_shift_invariance():
+    """Adding a vector c to every key of a head leaves out unchanged and shifts lse by q.c."""
+    rng = np.random.default_rng(8)
+    w = _small(seed=8, lens=(48, 33), ranges=[[(0, 48), (0, 33)]])
+    # small dyadic values keep k and k + c exactly representable in bf16
+    finite = np.isfinite(W.bf16_bits_to_f32(w.k_cache))
+    kq = rng.integers(-8, 9, size=w.k_cache.shape).astype(np.float32) / 8
+    w.k_cache[finite] = W.f32_to_bf16_bits(kq)[finite]
+    c = rng.integers(-16, 17, size=(2, 128)).astype(np.float32) / 8
+    w2 = W.make_custom(8, 2, 4, 2, [48, 33], [[(0, 48), (0, 33)]], q_scale=1.0 / math.sqrt(128))
+    w2.k_cache[...] = w.k_cache
+    shifted = W.bf16_bits_to_f32(w.k_cache) + c[None, :, None, :]
+    w2.k_cache[finite] = W.f32_to_bf16_bits(shifted)[finite]
+    assert np.array_equal(W.bf16_bits_to_f32(w2.k_cache)[finite], shifted[finite])
+    o1, l1 = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.kv_begin[0], w.kv_end[0])
+    o2, l2 = oracle.partial(w2.q, w2.k_cache, w2.v_cache, w2.block_table, w2.seq_lens, w2.kv_begin[0], w2.kv_end[0])
+    np.testing.assert_allclose(o2, o1, rtol=0, atol=1e-12)
+    for b in range(2):
+        for h in range(4):
+            qc = math.fsum((_f64(w.q[b, h]) * c[h // 2].astype(np.float64)).tolist())
+            assert abs(l2[b, h] - (l1[b, h] + qc)) < 1e-12
+
+
+def test_kv_rows_cover_each_token_once():
+    w = W.make_config("tiny", 7)
+    span = w.max_blocks_per_seq * 16
+    allrows = []
+    for p in range(w.n_parts):
+        rows = oracle.kv_rows(w.block_table, w.num_blocks, w.num_kv_heads, w.kv_begin[p], w.kv_end[p])
+        assert rows.shape == (w.batch, w.num_kv_heads, span)
+        for b in range(w.batch):
+            t = np.arange(span)
+            inside = (t >= w.kv_begin[p, b]) & (t < w.kv_end[p, b])
+            assert np.all(rows[b][:, ~inside] == -1)
+            assert np.all(rows[b][:, inside] >= 0)
+        allrows.append(rows)
+    rows = np.stack(allrows)
+    covered = rows[rows >= 0]
+    assert covered.size == len(np.unique(covered))  # no K row visited twice, across partitions too
+    assert covered.size == int(w.seq_lens.sum()) * w.num_kv_heads  # union = [0, L_b) for every head
+    kflat = W.bf16_bits_to_f32(w.k_cache).reshape(-1, 128)
+    assert np.all(np.isfinite(kflat[covered]))
+
+
+def test_oracle_rejects_unmapped_tokens():
+    w = _small(seed=9)
+    bad = w.block_table.copy()
+    bad[0, 1] = -1
+    with pytest.raises(ValueError):
+        oracle.partial(w.q, w.k_cache, w.v_cache, bad, w.seq_lens, w.kv_begin[1], w.kv_end[1])
