@@ -1,0 +1,228 @@
+#!/usr/bin/env python3
+"""Benchmark: split paged decode attention + merge on one MI355X.
+
+One step = every partition's ``bana_decode_attn_partial`` call plus the
+``bana_merge_partials`` call for one decode token of every sequence (one
+layer), on inputs already resident in HBM.  Default workload: the
+Llama-3-8B-shaped layer (batch 64, 32 query / 8 KV heads, head_dim 128,
+block 16, seq_len 4096, last 30 % of each sequence's blocks migrated ->
+2 partitions) over a 20 % oversized, randomly permuted block pool.
+
+Prints ONE JSON line.  ``value`` is the KV-read bandwidth of the whole step
+(K+V bytes of all covered tokens / step time); ``tokens_per_s`` is decode
+tokens (sequences) per second for the layer.  ``roofline`` reports the
+partial-attention kernel against the 8 TB/s HBM peak, timed with HIP events
+on the stream it runs on.  ``cpu_baseline`` times the fp64 CPU oracle on the
+same workload on this host.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "KV-read GB/s (% of HBM peak) and decode tokens/s, split paged attention"
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="llama3_8b", choices=["tiny", "llama3_8b", "long", "mixed", "fine"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU time of the oracle baseline")
+    ap.add_argument("--waves", type=int, default=0, help="waves-per-workgroup hint (0 = library plan)")
+    ap.add_argument("--chunks", type=int, default=0, help="chunks-per-range hint (0 = library plan)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device copy (for scaling HBM byte counters)")
+    return ap.parse_args()
+
+
+def _workload_desc(w):
+    nb = (w.kv_end - w.kv_begin).astype(np.int64)
+    return {
+        "workload": w.name,
+        "batch": w.batch,
+        "num_q_heads": w.num_q_heads,
+        "num_kv_heads": w.num_kv_heads,
+        "head_dim": 128,
+        "block_size": 16,
+        "seq_len_mean": float(np.mean(w.seq_lens)),
+        "partitions": w.n_parts,
+        "tokens_per_partition": [int(x) for x in nb.sum(axis=1)],
+        "pool_blocks": w.num_blocks,
+        "seed": w.seed,
+    }
+
+
+def _partial_algorithmic_bytes(w, p):
+    """Bytes one partial launch must move: K/V of covered tokens, q, table entries, fp32 out + lse."""
+    toks = int(np.sum(w.kv_end[p].astype(np.int64) - w.kv_begin[p]))
+    kv = toks * w.num_kv_heads * 128 * 2 * 2
+    blocks = 0
+    for b in range(w.batch):
+        t0, t1 = int(w.kv_begin[p, b]), int(w.kv_end[p, b])
+        if t1 > t0:
+            blocks += (t1 - 1) // 16 - t0 // 16 + 1
+    q = w.batch * w.num_q_heads * 128 * 2
+    out = w.batch * w.num_q_heads * (128 + 1) * 4
+    return kv + q + blocks * 4 + w.batch * 8 + out, kv
+
+
+def _cpu_baseline(w, target_s):
+    import oracle  # CPU baseline leg only
+
+    threads = len(os.sched_getaffinity(0))
+    reps = 0
+    t_start = time.perf_counter()
+    while True:
+        outs, lses = oracle.workload_partials(w, threads=threads)
+        oracle.merge(outs, lses)
+        reps += 1
+        el = time.perf_counter() - t_start
+        if el >= target_s or el / reps * (reps + 1) > 3 * target_s:
+            break
+    per_step = el / reps
+    kv = w.kv_bytes()
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {
+        "value": kv / per_step / 1e9,
+        "unit": "GB/s",
+        "tokens_per_s": w.batch / per_step,
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"full {w.name} step (all {w.n_parts} partitions of {w.batch} sequences + merge), "
+                  f"fp64, {reps} repetitions in {el:.1f} s",
+        "cpu_model": model,
+        "s_per_step": per_step,
+    }
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the method's partitions would shard across GPUs with one point-to-point exchange per step).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2510_13223_amd import workloads
+    from paper_2510_13223_amd.runner import DeviceWorkload
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t0 = time.time()
+    w = workloads.make_config(args.config, args.seed)
+    print(f"[bench] generated {w.name} in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    dw = DeviceWorkload(w, device=dev, waves_hint=args.waves, chunks_hint=args.chunks)
+    stream = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            dw.step(stream)
+    stream.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    P = w.n_parts
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(P)]
+          for _ in range(args.steps)]
+    step_start = torch.cuda.Event(enable_timing=True)
+    step_end = torch.cuda.Event(enable_timing=True)
+    h = __import__("ctypes").c_void_p(stream.cuda_stream)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    step_start.record(stream)
+    for k in range(args.steps):
+        for p in range(P):
+            ev[k][p][0].record(stream)
+            dw.partial(p, h)
+            ev[k][p][1].record(stream)
+        dw.merge(h)
+    step_end.record(stream)
+    stream.synchronize()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    gpu_ms = step_start.elapsed_time(step_end)
+    ms_per_step = wall * 1e3 / args.steps  # host wall clock, synchronised on both sides
+    print(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step", file=sys.stderr, flush=True)
+
+    kv_bytes = w.kv_bytes()
+    t_step = ms_per_step / 1e3
+    # Partial-attention kernel: algorithmic bytes over its own launch durations.
+    alg = [_partial_algorithmic_bytes(w, p) for p in range(P)]
+    dur_ms = np.array([[ev[k][p][0].elapsed_time(ev[k][p][1]) for p in range(P)] for k in range(args.steps)])
+    mean_dur_s = float(dur_ms.mean()) / 1e3
+    mean_bytes = float(np.mean([a[0] for a in alg]))
+    achieved = mean_bytes / mean_dur_s / 1e9
+    partial_kv_gbs = float(np.sum([a[1] for a in alg])) / (float(dur_ms.sum(axis=1).mean()) / 1e3) / 1e9
+
+    line = {
+        "metric": METRIC,
+        "value": round(kv_bytes / t_step / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "gpu_event_ms_per_step": round(gpu_ms / args.steps, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": _workload_desc(w),
+        "frac_of_hbm_peak": round(kv_bytes / t_step / 1e9 / HBM_PEAK_GBS, 4),
+        "tokens_per_s": round(w.batch / t_step, 1),
+        "tokens_per_s_32_layers": round(w.batch / (32 * t_step), 1),
+        "kv_bytes_per_step": kv_bytes,
+        "partial_kernels_kv_gbs": round(partial_kv_gbs, 2),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "partial_attn_kernel",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "algorithmic_bytes_per_launch": int(mean_bytes),
+            "mean_launch_us": round(mean_dur_s * 1e6, 2),
+            "launch_us_per_partition": [round(float(x) * 1e3, 2) for x in dur_ms.mean(axis=0)],
+        },
+    }
+    if args.copy_calibration:
+        n = 1 << 30
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        line["copy_calibration_bytes"] = n
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = _cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,149 @@
+/*
+ * bana.h -- C ABI of the split paged decode-attention library (libbana.so).
+ *
+ * The operation is the data-parallel step of attention-level KV-cache
+ * migration (paper: Sec. 4.1(2), "Attention-level migration"): a decode
+ * query attends to a paged KV cache whose token blocks are split into a
+ * local partition and one or more migrated partitions.  Each partition is
+ * reduced on its own to a softmax-normalised partial output plus its
+ * log-sum-exp (the per-partition S = Q K^T, A = exp S, l = sum A,
+ * O = A / l . V equations of that section), and a merge turns the partials
+ * into the exact softmax attention over all tokens (the section's final
+ * sum O = O^(1) + O^(2), with each partial rescaled by its share of the
+ * total denominator; l^(j) = exp(lse_j)).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - All tensor arguments are DEVICE pointers owned by the caller, resident
+ *    on the current HIP device, 16-byte aligned and densely packed in the
+ *    layouts stated below.  The library allocates no memory and keeps no
+ *    per-call state; calls are thread-safe.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream).  Nothing synchronises.
+ *  - Host-checkable argument errors return before any HIP call:
+ *    BANA_ERR_INVALID for a NULL required pointer, a non-positive size,
+ *    num_q_heads % num_kv_heads != 0, n_parts < 1 or a misaligned pointer;
+ *    BANA_ERR_UNSUPPORTED for head_dim != 128, block_size != 16 or a GQA
+ *    group (num_q_heads / num_kv_heads) above 16.
+ *  - A failed launch returns BANA_ERR_DEVICE; bana_last_error() then holds
+ *    the HIP error text (per calling thread).
+ *  - Device-resident values are preconditions and are not checked:
+ *    0 <= kv_range_begin[b] <= kv_range_end[b] <= seq_lens[b], and every
+ *    block-table entry for a block that overlaps [begin, end) names a block
+ *    of the pool.  Entries outside the covered blocks are never read.
+ *
+ * Layouts (bf16 = IEEE binary16-brain, stored as 2 bytes)
+ * --------------------------------------------------------
+ *   q            bf16  [batch][num_q_heads][head_dim]
+ *   k_cache      bf16  [num_blocks][num_kv_heads][block_size][head_dim]
+ *                      token-major 4 KiB tile per (block, kv head)
+ *   v_cache      bf16  [num_blocks][num_kv_heads][head_dim][block_size]
+ *                      dim-major 4 KiB tile per (block, kv head)
+ *   block_table  int32 [batch][max_blocks_per_seq]
+ *                      logical block j of sequence b -> physical block
+ *   seq_lens     int32 [batch]  tokens in the cache, current token included
+ *   out_partial  fp32  [batch][num_q_heads][head_dim]
+ *   lse          fp32  [batch][num_q_heads], natural log
+ *  Query head h reads kv head h / (num_q_heads / num_kv_heads).  Logical
+ *  token t of sequence b lives in block block_table[b][t / 16], slot t % 16.
+ *  Scores are the unscaled dot products q.k (the paper's S = Q K^T has no
+ *  1/sqrt(d) factor); a caller that wants a softmax scale pre-scales q.
+ */
+#ifndef BANA_H
+#define BANA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BANA_OK = 0,
+  BANA_ERR_INVALID = -1,
+  BANA_ERR_UNSUPPORTED = -2,
+  BANA_ERR_DEVICE = -3
+} bana_status;
+
+typedef struct {
+  int32_t batch;              /* B > 0 */
+  int32_t num_q_heads;        /* Hq > 0, a multiple of num_kv_heads */
+  int32_t num_kv_heads;       /* Hkv > 0; Hq / Hkv <= 16 */
+  int32_t head_dim;           /* 128 */
+  int32_t block_size;         /* 16 tokens per KV block */
+  int32_t max_blocks_per_seq; /* row stride of block_table */
+  int64_t num_blocks;         /* physical blocks in each pool */
+  /* Performance hints; 0 = let the library choose.  They never change
+   * results beyond float rounding order and never limit coverage. */
+  int32_t max_range_tokens;   /* upper bound of kv_range_end - kv_range_begin */
+  int32_t waves_hint;         /* waves per (sequence, kv head, chunk): 1, 2, 4 or 8 */
+  int32_t chunks_hint;        /* chunks a range may be split into (needs workspace) */
+  int32_t reserved;           /* must be 0 */
+} bana_dims;
+
+/*
+ * Partial attention of one partition (Sec. 4.1(2): one of "Atten for Local
+ * Seq" / "Atten for Offload Seq").  For every sequence b and query head h,
+ * over the logical tokens T = [kv_range_begin[b], kv_range_end[b]):
+ *   out_partial[b][h] = sum_{t in T} exp(s_t - m) v_t / sum_{t in T} exp(s_t - m)
+ *   lse[b][h]         = m + ln sum_{t in T} exp(s_t - m),   m = max_{t in T} s_t
+ * with s_t = q[b][h] . k_t.  An empty T gives out_partial = 0, lse = -inf.
+ * Ranges need not be block aligned.  bf16 inputs, fp32 accumulation.
+ *
+ * workspace: optional device scratch of workspace_bytes bytes, at least
+ * bana_decode_attn_workspace_bytes(d) for ranges to be split across several
+ * workgroups (long ranges, few sequences); with less (or NULL, 0) the call
+ * runs unsplit, with the same results up to rounding order.  The contents
+ * need no initialisation and are garbage afterwards.  Results are
+ * bit-identical run to run for the same inputs and dims, and invariant to
+ * the physical placement of blocks.
+ */
+bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
+                                     const int32_t* block_table, const int32_t* seq_lens,
+                                     const int32_t* kv_range_begin, const int32_t* kv_range_end,
+                                     float* out_partial, float* lse, void* workspace, size_t workspace_bytes,
+                                     void* stream);
+
+/* Bytes of workspace bana_decode_attn_partial can use for these dims (0 when
+ * it would not split ranges); 0 for invalid dims. */
+size_t bana_decode_attn_workspace_bytes(const bana_dims* d);
+
+/*
+ * Merge of n_parts partials (Sec. 4.1(2), final O = O^(1) + O^(2) with the
+ * exchange of the partial denominators l^(j) = exp(lse_j)).  Per row
+ * r = (b, h):  J = { p : lses[p][r] != -inf };  J empty -> out = 0,
+ * lse_out = -inf;  otherwise M = max_J lses[p][r], w_p = exp(lses[p][r] - M),
+ *   out[r]     = sum_J w_p out_partials[p][r] / sum_J w_p,
+ *   lse_out[r] = M + ln sum_J w_p.
+ * Rows of parts with lse = -inf are never read.  Summation runs in part order.
+ *   out_partials fp32 [n_parts][batch][num_q_heads][head_dim]
+ *   lses         fp32 [n_parts][batch][num_q_heads]
+ *   out          fp32 [batch][num_q_heads][head_dim]
+ *   lse_out      fp32 [batch][num_q_heads], or NULL
+ */
+bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, const float* lses, int32_t n_parts,
+                                float* out, float* lse_out, void* stream);
+
+/* Static text for a status code. */
+const char* bana_status_string(bana_status s);
+
+/* Text of the last HIP error seen by a call on this thread ("" if none). */
+const char* bana_last_error(void);
+
+/*
+ * Test hook for the address generator the attention kernel uses: for every
+ * sequence b, kv head g and logical token t < max_blocks_per_seq * 16,
+ *   rows_out[b][g][t] = (block_table[b][t / 16] * num_kv_heads + g) * 16 + t % 16
+ * (the K row the partial kernel reads for that token; V is read from the
+ * same (block, kv head) tile) when kv_range_begin[b] <= t < kv_range_end[b],
+ * and -1 otherwise.  rows_out: int64 [batch][num_kv_heads][max_blocks_per_seq * 16].
+ */
+bana_status bana_debug_kv_rows(const bana_dims* d, const int32_t* block_table, const int32_t* kv_range_begin,
+                               const int32_t* kv_range_end, int64_t* rows_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BANA_H */

@@ -1,0 +1,186 @@
+"""Python binding of libbana.so (ctypes).
+
+Argument marshalling only: every function checks tensor dtypes, shapes,
+devices and contiguity, then passes raw device pointers and the HIP stream
+handle to the C ABI declared in ``include/bana.h``.  All arithmetic runs in
+the library's HIP kernels; there is no fallback path, and a missing library
+raises.  PyTorch only provides device memory and streams.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libbana.so")
+
+HEAD_DIM = 128
+BLOCK_SIZE = 16
+
+BANA_OK = 0
+BANA_ERR_INVALID = -1
+BANA_ERR_UNSUPPORTED = -2
+BANA_ERR_DEVICE = -3
+
+
+class bana_dims(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("max_blocks_per_seq", ctypes.c_int32),
+        ("num_blocks", ctypes.c_int64),
+        ("max_range_tokens", ctypes.c_int32),
+        ("waves_hint", ctypes.c_int32),
+        ("chunks_hint", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+
+class BanaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        detail = lib().bana_last_error().decode() if status == BANA_ERR_DEVICE else ""
+        msg = f"{what}: {lib().bana_status_string(status).decode()} ({status})"
+        super().__init__(msg + (f": {detail}" if detail else ""))
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libbana.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2510_13223_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    D = ctypes.POINTER(bana_dims)
+    L.bana_decode_attn_partial.argtypes = [D, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    L.bana_decode_attn_partial.restype = ctypes.c_int
+    L.bana_decode_attn_workspace_bytes.argtypes = [D]
+    L.bana_decode_attn_workspace_bytes.restype = ctypes.c_size_t
+    L.bana_merge_partials.argtypes = [D, P, P, ctypes.c_int32, P, P, P]
+    L.bana_merge_partials.restype = ctypes.c_int
+    L.bana_status_string.argtypes = [ctypes.c_int]
+    L.bana_status_string.restype = ctypes.c_char_p
+    L.bana_last_error.argtypes = []
+    L.bana_last_error.restype = ctypes.c_char_p
+    L.bana_debug_kv_rows.argtypes = [D, P, P, P, P, P]
+    L.bana_debug_kv_rows.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def make_dims(batch: int, num_q_heads: int, num_kv_heads: int, max_blocks_per_seq: int, num_blocks: int,
+              max_range_tokens: int = 0, waves_hint: int = 0, chunks_hint: int = 0) -> bana_dims:
+    return bana_dims(batch, num_q_heads, num_kv_heads, HEAD_DIM, BLOCK_SIZE, max_blocks_per_seq, num_blocks,
+                     max_range_tokens, waves_hint, chunks_hint, 0)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor, got {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def dims_for(q: torch.Tensor, k_cache: torch.Tensor, block_table: torch.Tensor, max_range_tokens: int = 0,
+             waves_hint: int = 0, chunks_hint: int = 0) -> bana_dims:
+    B, Hq, D = q.shape
+    nb, Hkv, bs, D2 = k_cache.shape
+    return bana_dims(B, Hq, Hkv, D, bs, block_table.shape[1], nb, max_range_tokens, waves_hint, chunks_hint, 0)
+
+
+def bana_decode_attn_workspace_bytes(dims: bana_dims) -> int:
+    return int(lib().bana_decode_attn_workspace_bytes(ctypes.byref(dims)))
+
+
+def bana_decode_attn_partial(q, k_cache, v_cache, block_table, seq_lens, kv_range_begin, kv_range_end,
+                             out_partial, lse, workspace: Optional[torch.Tensor] = None, stream=None,
+                             dims: Optional[bana_dims] = None, max_range_tokens: int = 0) -> None:
+    """Partial attention of one partition; see ``bana_decode_attn_partial`` in include/bana.h."""
+    if q.dim() != 3 or k_cache.dim() != 4:
+        raise ValueError("q must be [B, Hq, D] and k_cache [num_blocks, Hkv, block_size, D]")
+    B, Hq, D = q.shape
+    nb, Hkv, bs, _ = k_cache.shape
+    _need(q, "q", torch.bfloat16)
+    _need(k_cache, "k_cache", torch.bfloat16, (nb, Hkv, bs, D))
+    _need(v_cache, "v_cache", torch.bfloat16, (nb, Hkv, D, bs))
+    _need(block_table, "block_table", torch.int32)
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError("block_table must be [B, max_blocks_per_seq]")
+    for name, t in (("seq_lens", seq_lens), ("kv_range_begin", kv_range_begin), ("kv_range_end", kv_range_end)):
+        _need(t, name, torch.int32, (B,))
+    _need(out_partial, "out_partial", torch.float32, (B, Hq, D))
+    _need(lse, "lse", torch.float32, (B, Hq))
+    ws_bytes = 0
+    if workspace is not None:
+        _need(workspace, "workspace", workspace.dtype)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    if dims is None:
+        dims = dims_for(q, k_cache, block_table, max_range_tokens)
+    st = lib().bana_decode_attn_partial(
+        ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens),
+        _ptr(kv_range_begin), _ptr(kv_range_end), _ptr(out_partial), _ptr(lse), _ptr(workspace), ws_bytes,
+        _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_decode_attn_partial")
+
+
+def bana_merge_partials(out_partials, lses, out, lse_out: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Log-sum-exp merge of ``out_partials [n_parts, B, Hq, D]`` / ``lses [n_parts, B, Hq]``."""
+    if out_partials.dim() != 4:
+        raise ValueError("out_partials must be [n_parts, B, Hq, D]")
+    n, B, Hq, D = out_partials.shape
+    _need(out_partials, "out_partials", torch.float32)
+    _need(lses, "lses", torch.float32, (n, B, Hq))
+    _need(out, "out", torch.float32, (B, Hq, D))
+    if lse_out is not None:
+        _need(lse_out, "lse_out", torch.float32, (B, Hq))
+    dims = bana_dims(B, Hq, 1, D, BLOCK_SIZE, 1, 1, 0, 0, 0, 0)
+    st = lib().bana_merge_partials(ctypes.byref(dims), _ptr(out_partials), _ptr(lses), n, _ptr(out), _ptr(lse_out),
+                                   _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_merge_partials")
+
+
+def bana_debug_kv_rows(block_table, kv_range_begin, kv_range_end, num_blocks: int, num_kv_heads: int, rows_out,
+                       stream=None) -> None:
+    """K rows the partial kernel reads per (b, g, t); see include/bana.h."""
+    B, mb = block_table.shape
+    _need(block_table, "block_table", torch.int32)
+    _need(kv_range_begin, "kv_range_begin", torch.int32, (B,))
+    _need(kv_range_end, "kv_range_end", torch.int32, (B,))
+    _need(rows_out, "rows_out", torch.int64, (B, num_kv_heads, mb * BLOCK_SIZE))
+    dims = bana_dims(B, num_kv_heads, num_kv_heads, HEAD_DIM, BLOCK_SIZE, mb, num_blocks, 0, 0, 0, 0)
+    st = lib().bana_debug_kv_rows(ctypes.byref(dims), _ptr(block_table), _ptr(kv_range_begin), _ptr(kv_range_end),
+                                  _ptr(rows_out), _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_debug_kv_rows")

@@ -1,0 +1,270 @@
+// attn_partial.hip -- partial attention of one KV partition over a paged cache (gfx950).
+//
+// Computes, per (sequence b, query head h) and over the logical tokens
+// [begin[b], end[b]) of one partition, the softmax-normalised partial output
+// and its log-sum-exp (paper Sec. 4.1(2): S = Q K^T, A = exp S, l = sum A,
+// O = A / l . V for one partition; the max-subtracted online form keeps the
+// same value in a finite range).
+//
+// Work decomposition.  One workgroup per (chunk c, sequence b, kv head g),
+// linearised chunk-major so that every (b, g) has its first chunk in the
+// first wave of dispatch.  A workgroup of W wavefronts walks the KV blocks of
+// its chunk round-robin (block jr goes to wave jr % W); each wavefront keeps
+// an online-softmax state for all G query heads of the kv head, and the W
+// states are combined through LDS at the end.  A range longer than one chunk
+// leaves one partial per chunk in caller workspace, merged by the merge
+// kernel with the same log-sum-exp algebra as the partition merge.
+//
+// One KV block (16 tokens x 128 dims for one kv head) per wavefront step:
+//   scores  S^T[16 tok x 16 col] = K[16 tok x 128] . Q^T[128 x 16 col]
+//           4 x v_mfma_f32_16x16x32_bf16, A = K rows straight from HBM
+//           (lane = token row, 16-byte loads), B = Q of the G heads of the
+//           group (columns >= G are zero).  bf16 x bf16 products are exact in
+//           fp32, accumulation is fp32.
+//   softmax running max per column (4 values per lane + two cross-lane
+//           shuffles), p = 2^((s - m) log2 e), rescale of the accumulator.
+//   values  O^T[128 dim x 16 col] += V^T[128 x 16 tok] . P^T[16 tok x 16 col]
+//           8 tiles of v_mfma_f32_16x16x16_bf16.  The score tile's output
+//           layout (lane = column, 4 consecutive token rows per lane) is
+//           exactly the B-operand layout of this product, so P never leaves
+//           its registers; V comes from the dim-major V tile with 8-byte loads
+//           (4 consecutive tokens of one dim).  P is split into a bf16 high
+//           part and a bf16 residual (two MFMAs per tile) so PV keeps ~16
+//           significant bits of P instead of bf16's 8.
+// Tokens of a partly covered block are selected out (score -inf, value 0),
+// never multiplied by zero, so NaN in unused slots cannot leak.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "kernels.h"
+#include "paged_addr.h"
+
+namespace bana {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kDimTiles = kHeadDim / 16;  // 8 output tiles of 16 dims
+constexpr int kRowPad = kHeadDim + 4;     // LDS row stride (floats) for the combine
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Max over the 4 lanes of a column (lanes l, l^16, l^32, l^48).
+__device__ __forceinline__ float column_max(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  x = fmaxf(x, __shfl_xor(x, 32));
+  return x;
+}
+
+__device__ __forceinline__ float column_sum(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+// p = hi + lo with hi = p truncated to bf16 (exact in fp32) and lo = bf16
+// round-to-nearest-even of the exact residual p - hi.  p is finite, >= 0.
+__device__ __forceinline__ void split_bf16(float p, uint32_t& hi, uint32_t& lo) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, p);
+  hi = u >> 16;
+  const float r = p - __builtin_bit_cast(float, u & 0xFFFF0000u);
+  const uint32_t ur = __builtin_bit_cast(uint32_t, r);
+  lo = (ur + 0x7FFFu + ((ur >> 16) & 1u)) >> 16;
+}
+
+template <int W>
+__global__ __launch_bounds__(64 * W) void partial_attn_kernel(PartialArgs a) {
+  extern __shared__ float smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int col = lane & 15;  // query head in group (score/output column); token row for K; dim for V
+  const int quad = lane >> 4;
+
+  int wg = blockIdx.x;
+  const int g = wg % a.Hkv;
+  wg /= a.Hkv;
+  const int b = wg % a.B;
+  const int c = wg / a.B;
+  const int G = a.G;
+  const int hq0 = g * G;
+
+  const int t0 = a.begin[b];
+  const int t1 = a.end[b];
+  int nblk = 0, jfirst = 0;
+  if (t1 > t0) {
+    jfirst = t0 >> 4;
+    nblk = ((t1 - 1) >> 4) - jfirst + 1;
+  }
+  int per = (nblk + a.nc - 1) / a.nc;
+  if (per < a.cmin) per = a.cmin;
+  const int nch = nblk > 0 ? (nblk + per - 1) / per : 0;
+
+  // Destination of this workgroup's result.
+  const int64_t row0 = ((int64_t)(a.nc == 1 ? 0 : c) * a.B + b) * a.Hq + hq0;
+  float* __restrict__ out_dst = a.out + row0 * kHeadDim;
+  float* __restrict__ lse_dst = a.lse + row0;
+
+  if (c >= nch) {  // empty range or chunk: out = 0, lse = -inf (chunk slots only need the lse)
+    if (a.nc == 1) {
+      for (int i = threadIdx.x; i < G * (kHeadDim / 4); i += 64 * W)
+        reinterpret_cast<f32x4*>(out_dst)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int i = threadIdx.x; i < G; i += 64 * W) lse_dst[i] = -INFINITY;
+    return;
+  }
+  const int jb0 = c * per;
+  const int jb1 = min(nblk, jb0 + per);
+
+  // B operand of the score product: Q^T, lane (col, quad) holds dims 32kk + 8quad + [0, 8) of head col.
+  bf16x8 qop[4];
+  {
+    const uint16_t* qrow = a.q + ((int64_t)b * a.Hq + hq0 + (col < G ? col : 0)) * kHeadDim + 8 * quad;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      u32x4 v = *reinterpret_cast<const u32x4*>(qrow + 32 * kk);
+      if (col >= G) v = u32x4{0u, 0u, 0u, 0u};
+      qop[kk] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  f32x4 acc[kDimTiles];
+#pragma unroll
+  for (int dt = 0; dt < kDimTiles; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY;
+  float lsum = 0.f;
+
+  for (int jr = jb0 + wave; jr < jb1; jr += W) {
+    const int j = jfirst + jr;
+    const int64_t tile = kv_tile(table_lookup(a.table, a.max_blocks, b, j), g, a.Hkv);
+    const uint16_t* __restrict__ kt = a.k + tile * kTileElems;
+    const uint16_t* __restrict__ vt = a.v + tile * kTileElems;
+
+    u32x4 kr[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      kr[kk] = *reinterpret_cast<const u32x4*>(kt + k_row(0, col) * kHeadDim + 32 * kk + 8 * quad);
+    u32x2 vr[kDimTiles];
+#pragma unroll
+    for (int dt = 0; dt < kDimTiles; ++dt)
+      vr[dt] = *reinterpret_cast<const u32x2*>(vt + (16 * dt + col) * kBlockSize + 4 * quad);
+
+    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[kk]), qop[kk], s, 0, 0, 0);
+    // s[i]: score of token slot 4*quad + i for head col.
+
+    if (j * kBlockSize < t0 || j * kBlockSize + kBlockSize > t1) {  // partly covered block (wave-uniform)
+      const int tok = j * kBlockSize + 4 * quad;
+      const bool ok0 = tok + 0 >= t0 && tok + 0 < t1;
+      const bool ok1 = tok + 1 >= t0 && tok + 1 < t1;
+      const bool ok2 = tok + 2 >= t0 && tok + 2 < t1;
+      const bool ok3 = tok + 3 >= t0 && tok + 3 < t1;
+      s[0] = ok0 ? s[0] : -INFINITY;
+      s[1] = ok1 ? s[1] : -INFINITY;
+      s[2] = ok2 ? s[2] : -INFINITY;
+      s[3] = ok3 ? s[3] : -INFINITY;
+      const uint32_t mlo = (ok0 ? 0x0000FFFFu : 0u) | (ok1 ? 0xFFFF0000u : 0u);
+      const uint32_t mhi = (ok2 ? 0x0000FFFFu : 0u) | (ok3 ? 0xFFFF0000u : 0u);
+#pragma unroll
+      for (int dt = 0; dt < kDimTiles; ++dt) {
+        vr[dt][0] &= mlo;
+        vr[dt][1] &= mhi;
+      }
+    }
+
+    const float mx = column_max(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])));
+    const float m_new = fmaxf(m, mx);  // finite: every visited block covers >= 1 token
+    const float alpha = fast_exp2((m - m_new) * kLog2e);
+    float p[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p[i] = fast_exp2((s[i] - m_new) * kLog2e);
+    lsum = lsum * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+    m = m_new;
+
+    uint32_t h0, l0, h1, l1, h2, l2, h3, l3;
+    split_bf16(p[0], h0, l0);
+    split_bf16(p[1], h1, l1);
+    split_bf16(p[2], h2, l2);
+    split_bf16(p[3], h3, l3);
+    const i16x4 phi = __builtin_bit_cast(i16x4, u32x2{h0 | (h1 << 16), h2 | (h3 << 16)});
+    const i16x4 plo = __builtin_bit_cast(i16x4, u32x2{l0 | (l1 << 16), l2 | (l3 << 16)});
+#pragma unroll
+    for (int dt = 0; dt < kDimTiles; ++dt) {
+      f32x4 t = acc[dt] * alpha;
+      const i16x4 va = __builtin_bit_cast(i16x4, vr[dt]);
+      t = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, phi, t, 0, 0, 0);
+      acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, plo, t, 0, 0, 0);
+    }
+  }
+  // acc[dt][i] = unnormalised output for dim 16dt + 4quad + i, head col; the
+  // per-lane lsum covers this lane's token rows only.
+  lsum = column_sum(lsum);
+
+  if (W == 1) {
+    if (col < G) {
+      const float inv = 1.0f / lsum;
+#pragma unroll
+      for (int dt = 0; dt < kDimTiles; ++dt)
+        *reinterpret_cast<f32x4*>(out_dst + col * kHeadDim + 16 * dt + 4 * quad) = acc[dt] * inv;
+      if (quad == 0) lse_dst[col] = m + logf(lsum);
+    }
+    return;
+  }
+
+  float* sm_m = smem;               // [W][16]
+  float* sm_l = smem + 16 * W;      // [W][16]
+  float* sm_acc = smem + 32 * W;    // [W][G][kRowPad]
+  if (quad == 0) {
+    sm_m[wave * 16 + col] = m;      // -inf for a wave that saw no block
+    sm_l[wave * 16 + col] = lsum;
+  }
+  if (col < G) {
+#pragma unroll
+    for (int dt = 0; dt < kDimTiles; ++dt)
+      *reinterpret_cast<f32x4*>(sm_acc + (wave * G + col) * kRowPad + 16 * dt + 4 * quad) = acc[dt];
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < G * (kHeadDim / 4); idx += 64 * W) {
+    const int h = idx >> 5;
+    const int d4 = idx & 31;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < W; ++w) M = fmaxf(M, sm_m[w * 16 + h]);
+    float L = 0.f;
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      const float mw = sm_m[w * 16 + h];
+      if (mw == -INFINITY) continue;
+      const float e = fast_exp2((mw - M) * kLog2e);
+      L += e * sm_l[w * 16 + h];
+      o += e * *reinterpret_cast<const f32x4*>(sm_acc + (w * G + h) * kRowPad + 4 * d4);
+    }
+    *reinterpret_cast<f32x4*>(out_dst + h * kHeadDim + 4 * d4) = o * (1.0f / L);
+    if (d4 == 0) lse_dst[h] = M + logf(L);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stream) {
+  const unsigned nwg = (unsigned)a.nc * (unsigned)a.B * (unsigned)a.Hkv;
+  const size_t smem = waves > 1 ? sizeof(float) * (size_t)(32 * waves + waves * a.G * kRowPad) : 0;
+  switch (waves) {
+    case 1: hipLaunchKernelGGL(partial_attn_kernel<1>, dim3(nwg), dim3(64), smem, stream, a); break;
+    case 2: hipLaunchKernelGGL(partial_attn_kernel<2>, dim3(nwg), dim3(128), smem, stream, a); break;
+    case 4: hipLaunchKernelGGL(partial_attn_kernel<4>, dim3(nwg), dim3(256), smem, stream, a); break;
+    case 8: hipLaunchKernelGGL(partial_attn_kernel<8>, dim3(nwg), dim3(512), smem, stream, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace bana

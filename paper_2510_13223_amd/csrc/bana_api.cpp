@@ -1,0 +1,188 @@
+// bana_api.cpp -- C ABI of libbana.so: argument checks, launch planning, launches.
+//
+// Every entry point validates what the host can see before touching HIP, so
+// a rejected call never reaches the device.  Launch plans are a pure
+// function of the dims (never of device properties or data), which keeps
+// results bit-identical across runs.
+#include "bana.h"
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <string>
+
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+constexpr int kHeadDim = 128;
+constexpr int kBlockSize = 16;
+constexpr int kMaxGroup = 16;           // query heads per kv head handled by one MFMA column tile
+constexpr int kTargetWaves = 256 * 16;  // 256 CUs x 16 resident wavefronts: one full dispatch round
+constexpr int kMaxBlocksPerWave = 64;   // longest run of blocks one wavefront should walk
+constexpr int kMaxChunks = 256;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bana_status check_dims(const bana_dims* d) {
+  if (d == nullptr) return BANA_ERR_INVALID;
+  if (d->batch <= 0 || d->num_q_heads <= 0 || d->num_kv_heads <= 0 || d->head_dim <= 0 || d->block_size <= 0 ||
+      d->max_blocks_per_seq <= 0 || d->num_blocks <= 0)
+    return BANA_ERR_INVALID;
+  if (d->num_q_heads % d->num_kv_heads != 0) return BANA_ERR_INVALID;
+  if (d->max_range_tokens < 0 || d->chunks_hint < 0 || d->reserved != 0) return BANA_ERR_INVALID;
+  if (d->waves_hint != 0 && d->waves_hint != 1 && d->waves_hint != 2 && d->waves_hint != 4 && d->waves_hint != 8)
+    return BANA_ERR_INVALID;
+  if (d->head_dim != kHeadDim || d->block_size != kBlockSize) return BANA_ERR_UNSUPPORTED;
+  if (d->num_q_heads / d->num_kv_heads > kMaxGroup) return BANA_ERR_UNSUPPORTED;
+  // Index arithmetic of the kernels: table rows and token indices are 32-bit.
+  if ((int64_t)d->batch * d->max_blocks_per_seq > INT32_MAX ||
+      (int64_t)d->max_blocks_per_seq * kBlockSize > INT32_MAX)
+    return BANA_ERR_UNSUPPORTED;
+  return BANA_OK;
+}
+
+struct Plan {
+  int waves;  // wavefronts per workgroup
+  int nc;     // chunks per (sequence, kv head)
+  int cmin;   // minimum blocks per chunk
+};
+
+int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+// Workgroups are (chunk, sequence, kv head).  Aim for one full round of
+// resident wavefronts over all (sequence, kv head) pairs, give every
+// wavefront at least a few blocks, and cut long ranges into chunks so no
+// wavefront walks more than kMaxBlocksPerWave blocks.
+Plan make_plan(const bana_dims* d) {
+  const int64_t pairs = (int64_t)d->batch * d->num_kv_heads;
+  int64_t bound = d->max_blocks_per_seq;
+  if (d->max_range_tokens > 0) bound = std::min<int64_t>(bound, (d->max_range_tokens + kBlockSize - 1) / kBlockSize + 1);
+  int64_t wpp = (kTargetWaves + pairs - 1) / pairs;
+  wpp = std::max<int64_t>(1, std::min<int64_t>(wpp, std::max<int64_t>(1, bound / 4)));
+  Plan p;
+  if (d->waves_hint > 0)
+    p.waves = d->waves_hint;
+  else
+    p.waves = wpp >= 8 ? 8 : wpp >= 4 ? 4 : wpp >= 2 ? 2 : 1;
+  // The cross-wave combine keeps W * G rows of 132 floats in LDS; stay within 64 KiB per workgroup.
+  const int G = d->num_q_heads / d->num_kv_heads;
+  while (p.waves > 1 && sizeof(float) * (size_t)(32 * p.waves + p.waves * G * (kHeadDim + 4)) > 65536) p.waves /= 2;
+  if (d->chunks_hint > 0) {
+    p.nc = d->chunks_hint;
+    p.cmin = 1;
+  } else {
+    p.nc = std::max(ceil_div(wpp, p.waves), ceil_div(bound, (int64_t)p.waves * kMaxBlocksPerWave));
+    p.cmin = p.waves * 16;
+  }
+  p.nc = std::max(1, std::min(p.nc, kMaxChunks));
+  if ((int64_t)p.nc * pairs > INT32_MAX) p.nc = 1;
+  return p;
+}
+
+size_t workspace_for(const bana_dims* d, int nc) {
+  if (nc <= 1) return 0;
+  const size_t rows = (size_t)nc * d->batch * d->num_q_heads;
+  const size_t bytes = rows * kHeadDim * sizeof(float) + rows * sizeof(float);
+  return (bytes + 255) & ~(size_t)255;
+}
+
+bana_status device_status(hipError_t e) {
+  if (e == hipSuccess) return BANA_OK;
+  g_last_error = hipGetErrorString(e);
+  return BANA_ERR_DEVICE;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* bana_status_string(bana_status s) {
+  switch (s) {
+    case BANA_OK: return "ok";
+    case BANA_ERR_INVALID: return "invalid argument";
+    case BANA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case BANA_ERR_DEVICE: return "device error";
+  }
+  return "unknown status";
+}
+
+const char* bana_last_error(void) { return g_last_error.c_str(); }
+
+size_t bana_decode_attn_workspace_bytes(const bana_dims* d) {
+  if (check_dims(d) != BANA_OK) return 0;
+  return workspace_for(d, make_plan(d).nc);
+}
+
+bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
+                                     const int32_t* block_table, const int32_t* seq_lens,
+                                     const int32_t* kv_range_begin, const int32_t* kv_range_end,
+                                     float* out_partial, float* lse, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !kv_range_begin || !kv_range_end || !out_partial ||
+      !lse)
+    return BANA_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out_partial) ||
+      (workspace != nullptr && !aligned16(workspace)))
+    return BANA_ERR_INVALID;
+
+  Plan plan = make_plan(d);
+  const size_t need = workspace_for(d, plan.nc);
+  if (plan.nc > 1 && (workspace == nullptr || workspace_bytes < need)) plan.nc = 1;
+
+  bana::PartialArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k_cache);
+  a.v = static_cast<const uint16_t*>(v_cache);
+  a.table = block_table;
+  a.begin = kv_range_begin;
+  a.end = kv_range_end;
+  a.B = d->batch;
+  a.Hq = d->num_q_heads;
+  a.Hkv = d->num_kv_heads;
+  a.G = d->num_q_heads / d->num_kv_heads;
+  a.max_blocks = d->max_blocks_per_seq;
+  a.nc = plan.nc;
+  a.cmin = plan.cmin;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t rows = (int64_t)d->batch * d->num_q_heads;
+  if (plan.nc == 1) {
+    a.out = out_partial;
+    a.lse = lse;
+    return device_status(bana::launch_partial_attn(a, plan.waves, s));
+  }
+  float* ws_out = static_cast<float*>(workspace);
+  float* ws_lse = ws_out + (size_t)plan.nc * rows * kHeadDim;
+  a.out = ws_out;
+  a.lse = ws_lse;
+  hipError_t e = bana::launch_partial_attn(a, plan.waves, s);
+  if (e != hipSuccess) return device_status(e);
+  return device_status(bana::launch_merge(ws_out, ws_lse, plan.nc, rows, out_partial, lse, s));
+}
+
+bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, const float* lses, int32_t n_parts,
+                                float* out, float* lse_out, void* stream) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!out_partials || !lses || !out || n_parts < 1) return BANA_ERR_INVALID;
+  if (!aligned16(out_partials) || !aligned16(out)) return BANA_ERR_INVALID;
+  const int64_t rows = (int64_t)d->batch * d->num_q_heads;
+  return device_status(
+      bana::launch_merge(out_partials, lses, n_parts, rows, out, lse_out, static_cast<hipStream_t>(stream)));
+}
+
+bana_status bana_debug_kv_rows(const bana_dims* d, const int32_t* block_table, const int32_t* kv_range_begin,
+                               const int32_t* kv_range_end, int64_t* rows_out, void* stream) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!block_table || !kv_range_begin || !kv_range_end || !rows_out) return BANA_ERR_INVALID;
+  return device_status(bana::launch_debug_rows(block_table, kv_range_begin, kv_range_end, d->batch, d->num_kv_heads,
+                                               d->max_blocks_per_seq, rows_out, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

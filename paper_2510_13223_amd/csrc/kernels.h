@@ -1,0 +1,35 @@
+// kernels.h -- host-side launchers of the HIP kernels (internal to libbana.so).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bana {
+
+struct PartialArgs {
+  const uint16_t* q;        // bf16 [B][Hq][128]
+  const uint16_t* k;        // bf16 [num_blocks][Hkv][16][128]
+  const uint16_t* v;        // bf16 [num_blocks][Hkv][128][16]
+  const int32_t* table;     // [B][max_blocks]
+  const int32_t* begin;     // [B]
+  const int32_t* end;       // [B]
+  float* out;               // nc == 1: final out_partial [B][Hq][128]; nc > 1: chunk partials [nc][B][Hq][128]
+  float* lse;               // nc == 1: final lse [B][Hq];               nc > 1: chunk lses [nc][B][Hq]
+  int B, Hq, Hkv, G, max_blocks;
+  int nc;    // chunks per (sequence, kv head)
+  int cmin;  // minimum blocks per chunk
+};
+
+// Partial attention: one workgroup of `waves` wavefronts per (chunk, sequence, kv head).
+hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stream);
+
+// Log-sum-exp merge of n_parts partials over `rows` rows of 128 floats.
+hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t rows, float* out, float* lse_out,
+                        hipStream_t stream);
+
+// Address export for the tests (rows of the K pool visited per logical token).
+hipError_t launch_debug_rows(const int32_t* table, const int32_t* begin, const int32_t* end, int B, int Hkv,
+                             int max_blocks, int64_t* rows, hipStream_t stream);
+
+}  // namespace bana

@@ -1,0 +1,30 @@
+// paged_addr.h -- device-side address generation for the paged KV cache.
+//
+// Shared by the partial-attention kernel and the address-export test kernel
+// so that the rows the test sees are the rows the attention reads.  Layout:
+// K pool [num_blocks][Hkv][16][128] (token-major tile per (block, kv head)),
+// V pool [num_blocks][Hkv][128][16] (dim-major tile per (block, kv head)).
+#pragma once
+
+#include <stdint.h>
+
+namespace bana {
+
+constexpr int kHeadDim = 128;
+constexpr int kBlockSize = 16;
+constexpr int kTileElems = kHeadDim * kBlockSize;  // bf16 elements per (block, kv head) tile
+
+// Physical block of logical block j of sequence b.
+__device__ __forceinline__ int32_t table_lookup(const int32_t* __restrict__ table, int max_blocks, int b, int j) {
+  return table[(int64_t)b * max_blocks + j];
+}
+
+// Index of the (block, kv head) tile; the tile starts at tile * kTileElems in either pool.
+__device__ __forceinline__ int64_t kv_tile(int32_t blk, int g, int num_kv_heads) {
+  return (int64_t)blk * num_kv_heads + g;
+}
+
+// K row (in units of kHeadDim elements) of slot `slot` of a tile.
+__device__ __forceinline__ int64_t k_row(int64_t tile, int slot) { return tile * kBlockSize + slot; }
+
+}  // namespace bana

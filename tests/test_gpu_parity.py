@@ -1,0 +1,266 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Tolerances (fp32 outputs of bf16-in / fp32-accumulate kernels), over each
+config's whole output tensor: max-abs error <= 2e-3 and relative L2 error
+<= 1e-3 for every partition's out_partial and for the merged out; |dlse| <=
+1e-4 on finite entries, and -inf exactly where a partition is empty.
+Indexing and coverage are checked bit-exactly: the exported K rows equal the
+oracle's, zero keys give round(exp(lse)) == range length, and a dominant key
+returns its value row exactly.
+"""
+
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2510_13223_amd import bana, workloads as W
+from paper_2510_13223_amd.runner import DeviceWorkload
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS = 2e-3
+REL_L2 = 1e-3
+LSE_ABS = 1e-4
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    bana.lib()  # raises if the HIP library is missing: there is no fallback
+    yield
+
+
+_CACHE = {}
+
+
+def _workload(name, seed=0):
+    key = (name, seed)
+    if key not in _CACHE:
+        if len(_CACHE) >= 2:
+            _CACHE.clear()
+        _CACHE[key] = W.make_config(name, seed)
+    return _CACHE[key]
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _check_out(gpu, ref, what):
+    gpu = gpu.astype(np.float64)
+    assert np.all(np.isfinite(gpu)), f"{what}: non-finite output"
+    diff = gpu - ref
+    max_abs = float(np.max(np.abs(diff))) if diff.size else 0.0
+    rel = float(np.linalg.norm(diff) / max(np.linalg.norm(ref), 1e-300)) if diff.size else 0.0
+    assert max_abs <= MAX_ABS, f"{what}: max-abs {max_abs:.3e}"
+    assert rel <= REL_L2, f"{what}: rel-L2 {rel:.3e}"
+    return max_abs, rel
+
+
+def _check_lse(gpu, ref, what):
+    gpu = gpu.astype(np.float64)
+    ninf = np.isneginf(ref)
+    assert np.array_equal(np.isneginf(gpu), ninf), f"{what}: -inf pattern differs"
+    fin = ~ninf
+    assert np.all(np.isfinite(gpu[fin])), f"{what}: non-finite lse"
+    err = float(np.max(np.abs(gpu[fin] - ref[fin]))) if fin.any() else 0.0
+    assert err <= LSE_ABS, f"{what}: lse max-abs {err:.3e}"
+    return err
+
+
+def _full_parity(w, **kw):
+    _log(f"[parity] {w.name} seed={w.seed} B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} parts={w.n_parts} {kw}")
+    dw = DeviceWorkload(w, **kw)
+    op, lp, out, lse_out = dw.results()
+    ro, rl = oracle.workload_partials(w)
+    for p in range(w.n_parts):
+        _check_out(op[p][np.isfinite(rl[p])], ro[p][np.isfinite(rl[p])], f"{w.name} part {p} out_partial")
+        assert np.all(op[p][np.isneginf(rl[p])] == 0.0), "empty partition must give out_partial = 0"
+        _check_lse(lp[p], rl[p], f"{w.name} part {p}")
+    mo, ml = oracle.merge(ro, rl)
+    uo, ul = oracle.workload_unsplit(w)
+    np.testing.assert_allclose(mo, uo, rtol=0, atol=1e-10)  # oracle's own merge == unsplit
+    stats = _check_out(out, uo, f"{w.name} merged out")
+    _check_lse(lse_out, ul, f"{w.name} merged lse")
+    _log(f"  merged max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
+    return dw
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_tiny_parity(seed):
+    _full_parity(_workload("tiny", seed))
+
+
+@pytest.mark.parametrize("name", ["llama3_8b", "long", "mixed", "fine"])
+def test_config_parity(name):
+    _full_parity(_workload(name))
+
+
+@pytest.mark.parametrize("waves,chunks", [(1, 1), (2, 3), (4, 1), (8, 2), (1, 7), (8, 16)])
+def test_launch_plans_agree(waves, chunks):
+    """Every launch shape (waves per workgroup, chunks per range) meets the same bar."""
+    w = _workload("tiny", 1)
+    _full_parity(w, waves_hint=waves, chunks_hint=chunks)
+
+
+def test_without_workspace_runs_unsplit():
+    w = _workload("tiny", 2)
+    _full_parity(w, use_workspace=False, range_hints=False)
+
+
+def test_run_to_run_bit_determinism():
+    w = _workload("tiny", 0)
+    dw = DeviceWorkload(w)
+    a = dw.results()
+    dw.step()
+    b = dw.results()
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y, equal_nan=True)
+
+
+def test_physical_block_permutation_bit_identical():
+    w = _workload("tiny", 0)
+    a = DeviceWorkload(w).results()
+    b = DeviceWorkload(W.permute_physical(w, 3)).results()
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y, equal_nan=True)
+
+
+def test_debug_rows_bit_exact():
+    for name in ("tiny", "mixed"):
+        w = _workload(name)
+        _log(f"[rows] {name}")
+        dw = DeviceWorkload(w)
+        for p in range(w.n_parts):
+            rows = torch.empty((w.batch, w.num_kv_heads, w.max_blocks_per_seq * 16), dtype=torch.int64, device="cuda")
+            bana.bana_debug_kv_rows(dw.block_table, dw.kv_begin[p], dw.kv_end[p], w.num_blocks, w.num_kv_heads, rows)
+            ref = oracle.kv_rows(w.block_table, w.num_blocks, w.num_kv_heads, w.kv_begin[p], w.kv_end[p])
+            np.testing.assert_array_equal(rows.cpu().numpy(), ref)
+
+
+def _aim_dominant(w, part, seed):
+    """Per (b, g): one key in the partition aimed along head g*G's query so it wins by > 110."""
+    rng = np.random.default_rng(seed)
+    G = w.group
+    chosen = {}
+    for b in range(w.batch):
+        t0, t1 = int(w.kv_begin[part, b]), int(w.kv_end[part, b])
+        if t1 <= t0:
+            continue
+        for g in range(w.num_kv_heads):
+            t = int(rng.integers(t0, t1))
+            qf = W.bf16_bits_to_f32(w.q[b, g * G]).astype(np.float32)
+            scale = np.float32(300.0 / float(qf @ qf))
+            blk = w.block_table[b, t // 16]
+            w.k_cache[blk, g, t % 16, :] = W.f32_to_bf16_bits(qf * scale)
+            chosen[(b, g)] = t
+    return chosen
+
+
+@pytest.mark.parametrize("waves,chunks", [(0, 0), (1, 1), (8, 3)])
+def test_dominant_key_returns_value_row_exactly(waves, chunks):
+    w = W.make_config("tiny", 3)
+    chosen = {part: _aim_dominant(w, part, 10 + part) for part in range(w.n_parts)}
+    _log(f"[dominant] waves={waves} chunks={chunks}")
+    op, lp, _, _ = DeviceWorkload(w, waves_hint=waves, chunks_hint=chunks).results()
+    for part, picks in chosen.items():
+        for (b, g), t in picks.items():
+            blk = w.block_table[b, t // 16]
+            v = W.bf16_bits_to_f32(w.v_cache[blk, g, :, t % 16])
+            assert np.array_equal(op[part, b, g * w.group], v), (part, b, g, t)
+
+
+def test_zero_keys_pin_coverage_counts():
+    for name, kw in (("tiny", {}), ("tiny", dict(waves_hint=4, chunks_hint=5)), ("mixed", {})):
+        w = W.make_config(name, 0)
+        finite = np.isfinite(W.bf16_bits_to_f32(w.k_cache))
+        w.k_cache[finite] = 0
+        _log(f"[coverage] {name} {kw}")
+        op, lp, out, lse_out = DeviceWorkload(w, **kw).results()
+        n = (w.kv_end - w.kv_begin).astype(np.float64)[:, :, None].repeat(w.num_q_heads, 2)
+        live = n > 0
+        assert np.array_equal(np.rint(np.exp(lp[live].astype(np.float64))), n[live])
+        assert np.all(np.isneginf(lp[~live]))
+        assert np.array_equal(np.rint(np.exp(lse_out.astype(np.float64))),
+                              w.seq_lens.astype(np.float64)[:, None].repeat(w.num_q_heads, 1))
+
+
+def test_single_key_and_non_aligned_ranges():
+    lens = [37, 64, 300, 17, 1]
+    ranges = [
+        [(17, 18), (63, 64), (5, 299), (0, 17), (0, 0)],
+        [(0, 17), (0, 63), (299, 300), (17, 17), (0, 1)],
+        [(18, 37), (0, 0), (0, 5), (0, 0), (1, 1)],
+    ]
+    w = W.make_custom(4, 5, 8, 2, lens, ranges, q_scale=1 / math.sqrt(128))
+    dw = _full_parity(w)
+    op, _, _, _ = dw.results()
+    for part, b, t in ((0, 0, 17), (0, 1, 63), (1, 2, 299), (1, 4, 0)):
+        for h in range(8):
+            blk = w.block_table[b, t // 16]
+            v = W.bf16_bits_to_f32(w.v_cache[blk, h // 4, :, t % 16])
+            assert np.array_equal(op[part, b, h], v)
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (8, 4), (32, 2), (12, 4)])
+def test_other_gqa_groups(Hq, Hkv):
+    rng = np.random.default_rng(Hq * 100 + Hkv)
+    lens = rng.integers(1, 700, size=6)
+    ranges = [[], []]
+    for L in lens:
+        cut = int(rng.integers(0, L + 1))
+        ranges[0].append((0, cut))
+        ranges[1].append((cut, int(L)))
+    w = W.make_custom(11, 6, Hq, Hkv, lens, ranges, q_scale=1 / math.sqrt(128))
+    _full_parity(w)
+
+
+def test_scaled_query_reading_llama_shape():
+    """Alternative reading with a 1/sqrt(128) softmax scale folded into q (config-2 shape, 8 sequences)."""
+    lens = [4096] * 8
+    ranges = [[(0, 179 * 16)] * 8, [(179 * 16, 4096)] * 8]
+    w = W.make_custom(2, 8, 32, 8, lens, ranges, max_blocks_per_seq=256, q_scale=1 / math.sqrt(128))
+    _full_parity(w)
+
+
+def test_merge_matches_oracle_merge():
+    rng = np.random.default_rng(0)
+    n, B, Hq = 5, 7, 8
+    outs = rng.standard_normal((n, B, Hq, 128)).astype(np.float32)
+    lses = (rng.standard_normal((n, B, Hq)) * 20).astype(np.float32)
+    lses[rng.random((n, B, Hq)) < 0.3] = -np.inf
+    lses[:, 0, 0] = -np.inf  # an all-empty row
+    outs[np.isneginf(lses)] = np.nan  # rows of empty parts are never read
+    d_out = torch.empty((B, Hq, 128), dtype=torch.float32, device="cuda")
+    d_lse = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+    bana.bana_merge_partials(torch.from_numpy(outs).cuda(), torch.from_numpy(lses).cuda(), d_out, d_lse)
+    ro, rl = oracle.merge(outs.astype(np.float64), lses.astype(np.float64))
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(d_out.cpu().numpy(), ro, rtol=0, atol=1e-5)
+    got = d_lse.cpu().numpy()
+    assert np.array_equal(np.isneginf(got), np.isneginf(rl))
+    np.testing.assert_allclose(got[np.isfinite(rl)], rl[np.isfinite(rl)], rtol=0, atol=1e-5)
+    assert np.all(d_out.cpu().numpy()[0, 0] == 0)
+
+
+def test_non_default_stream_and_binding_checks():
+    w = _workload("tiny", 0)
+    ref = DeviceWorkload(w).results()
+    dw = DeviceWorkload(w)
+    dw.out.zero_()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        dw.step(s)
+    s.synchronize()
+    got = dw.results()
+    for x, y in zip(ref, got):
+        assert np.array_equal(x, y, equal_nan=True)
+    with pytest.raises(TypeError):
+        bana.bana_decode_attn_partial(dw.q.float(), dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens,
+                                      dw.kv_begin[0], dw.kv_end[0], dw.out_partials[0], dw.lses[0])

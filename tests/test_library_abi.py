@@ -1,0 +1,116 @@
+"""CPU checks of libbana.so: it loads, exports every declared symbol, and rejects
+bad arguments on the host before any HIP call (no compute call needs a GPU)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2510_13223_amd import bana
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bana.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bana_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(bana.LIB_PATH):
+        from paper_2510_13223_amd import build
+        build.build()
+    return bana.lib()
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for n in ("bana_decode_attn_partial", "bana_merge_partials", "bana_decode_attn_workspace_bytes",
+              "bana_status_string", "bana_last_error", "bana_debug_kv_rows"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for n in _declared_functions():
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    assert lib.bana_status_string(0) == b"ok"
+    assert lib.bana_status_string(-1) == b"invalid argument"
+    assert lib.bana_status_string(-2) == b"unsupported configuration"
+    assert lib.bana_status_string(-3) == b"device error"
+    assert lib.bana_last_error() == b""
+
+
+def _dims(**kw):
+    base = dict(batch=4, num_q_heads=8, num_kv_heads=2, max_blocks_per_seq=64, num_blocks=100)
+    base.update(kw)
+    d = bana.make_dims(base["batch"], base["num_q_heads"], base["num_kv_heads"], base["max_blocks_per_seq"],
+                       base["num_blocks"])
+    for k in ("head_dim", "block_size", "reserved", "waves_hint", "chunks_hint", "max_range_tokens"):
+        if k in kw:
+            setattr(d, k, kw[k])
+    return d
+
+
+FAKE = ctypes.c_void_p(0x100000)  # 16-byte aligned, never dereferenced: every case below fails validation
+
+
+def _partial(lib, d, ptrs=None, ws=None, ws_bytes=0):
+    p = ptrs or [FAKE] * 9
+    return lib.bana_decode_attn_partial(ctypes.byref(d) if d is not None else None, *p, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(batch=0), -1), (dict(num_q_heads=-8), -1), (dict(num_kv_heads=3), -1), (dict(num_blocks=0), -1),
+    (dict(max_blocks_per_seq=0), -1), (dict(reserved=1), -1), (dict(waves_hint=3), -1), (dict(chunks_hint=-1), -1),
+    (dict(max_range_tokens=-5), -1),
+    (dict(head_dim=64), -2), (dict(block_size=32), -2), (dict(num_q_heads=34, num_kv_heads=2), -2),
+])
+def test_partial_rejects_bad_dims(lib, kw, expect):
+    assert _partial(lib, _dims(**kw)) == expect
+    assert lib.bana_decode_attn_workspace_bytes(ctypes.byref(_dims(**kw))) == 0
+
+
+def test_partial_rejects_null_and_misaligned(lib):
+    assert _partial(lib, None) == -1
+    for i in range(9):
+        ptrs = [FAKE] * 9
+        ptrs[i] = None
+        assert _partial(lib, _dims(), ptrs) == -1, i
+    for i in (0, 1, 2, 7):  # q, k_cache, v_cache, out_partial must be 16-byte aligned
+        ptrs = [FAKE] * 9
+        ptrs[i] = ctypes.c_void_p(0x100008)
+        assert _partial(lib, _dims(), ptrs) == -1, i
+    assert _partial(lib, _dims(), None, ctypes.c_void_p(0x100004), 4096) == -1
+
+
+def test_merge_rejects_bad_arguments(lib):
+    d = _dims()
+    assert lib.bana_merge_partials(ctypes.byref(d), FAKE, FAKE, 0, FAKE, None, None) == -1
+    assert lib.bana_merge_partials(ctypes.byref(d), None, FAKE, 2, FAKE, None, None) == -1
+    assert lib.bana_merge_partials(ctypes.byref(d), FAKE, None, 2, FAKE, None, None) == -1
+    assert lib.bana_merge_partials(ctypes.byref(d), FAKE, FAKE, 2, None, None, None) == -1
+    assert lib.bana_merge_partials(ctypes.byref(d), ctypes.c_void_p(0x100004), FAKE, 2, FAKE, None, None) == -1
+    assert lib.bana_merge_partials(ctypes.byref(_dims(head_dim=96)), FAKE, FAKE, 2, FAKE, None, None) == -2
+    assert lib.bana_debug_kv_rows(ctypes.byref(d), None, FAKE, FAKE, FAKE, None) == -1
+
+
+def test_workspace_sizing_follows_the_plan(lib):
+    # 64 sequences x 8 kv heads fill the GPU with one chunk per (sequence, kv head): no workspace
+    d = bana.make_dims(64, 32, 8, 256, 19661, max_range_tokens=2864)
+    assert lib.bana_decode_attn_workspace_bytes(ctypes.byref(d)) == 0
+    # 8 sequences x 8 kv heads of long ranges: split into chunks, one fp32 row + lse per chunk row
+    d = bana.make_dims(8, 32, 8, 8192, 50000, max_range_tokens=60000)
+    ws = lib.bana_decode_attn_workspace_bytes(ctypes.byref(d))
+    assert ws > 0 and ws % 256 == 0
+    nc = round(ws / (8 * 32 * 129 * 4))
+    assert nc >= 2 and ws >= nc * 8 * 32 * 129 * 4
+    # an explicit chunk hint sizes the workspace exactly
+    d = bana.make_dims(8, 32, 8, 8192, 50000, chunks_hint=4)
+    assert lib.bana_decode_attn_workspace_bytes(ctypes.byref(d)) == (4 * 8 * 32 * 129 * 4 + 255) // 256 * 256
