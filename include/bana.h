@@ -117,6 +117,7 @@ size_t bana_decode_attn_workspace_bytes(const bana_dims* d);
  *   out[r]     = sum_J w_p out_partials[p][r] / sum_J w_p,
  *   lse_out[r] = M + ln sum_J w_p.
  * Rows of parts with lse = -inf are never read.  Summation runs in part order.
+ * Of d, only batch, num_q_heads and head_dim are read.
  *   out_partials fp32 [n_parts][batch][num_q_heads][head_dim]
  *   lses         fp32 [n_parts][batch][num_q_heads]
  *   out          fp32 [batch][num_q_heads][head_dim]

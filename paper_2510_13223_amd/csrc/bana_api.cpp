@@ -167,8 +167,9 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
 
 bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, const float* lses, int32_t n_parts,
                                 float* out, float* lse_out, void* stream) {
-  const bana_status st = check_dims(d);
-  if (st != BANA_OK) return st;
+  // Only the row count (batch x num_q_heads) and head_dim matter to the merge.
+  if (d == nullptr || d->batch <= 0 || d->num_q_heads <= 0 || d->head_dim <= 0) return BANA_ERR_INVALID;
+  if (d->head_dim != kHeadDim) return BANA_ERR_UNSUPPORTED;
   if (!out_partials || !lses || !out || n_parts < 1) return BANA_ERR_INVALID;
   if (!aligned16(out_partials) || !aligned16(out)) return BANA_ERR_INVALID;
   const int64_t rows = (int64_t)d->batch * d->num_q_heads;

@@ -98,6 +98,8 @@ def test_merge_rejects_bad_arguments(lib):
     assert lib.bana_merge_partials(ctypes.byref(d), FAKE, FAKE, 2, None, None, None) == -1
     assert lib.bana_merge_partials(ctypes.byref(d), ctypes.c_void_p(0x100004), FAKE, 2, FAKE, None, None) == -1
     assert lib.bana_merge_partials(ctypes.byref(_dims(head_dim=96)), FAKE, FAKE, 2, FAKE, None, None) == -2
+    assert lib.bana_merge_partials(ctypes.byref(_dims(batch=0)), FAKE, FAKE, 2, FAKE, None, None) == -1
+    assert lib.bana_merge_partials(None, FAKE, FAKE, 2, FAKE, None, None) == -1
     assert lib.bana_debug_kv_rows(ctypes.byref(d), None, FAKE, FAKE, FAKE, None) == -1
 
 
