@@ -14,9 +14,13 @@ constexpr int kHeadDim = 128;
 constexpr int kBlockSize = 16;
 constexpr int kTileElems = kHeadDim * kBlockSize;  // bf16 elements per (block, kv head) tile
 
-// Physical block of logical block j of sequence b.
+// Physical block of logical block j of sequence b.  The table is read-only
+// for the whole launch and b, j are wave-uniform, so the entry is read
+// through the constant address space: one scalar load per wave, tracked
+// apart from the vector loads of K and V (it never stalls their pipeline).
 __device__ __forceinline__ int32_t table_lookup(const int32_t* __restrict__ table, int max_blocks, int b, int j) {
-  return table[(int64_t)b * max_blocks + j];
+  typedef const __attribute__((address_space(4))) int32_t* const_ptr;
+  return ((const_ptr)table)[(int64_t)b * max_blocks + j];
 }
 
 // Index of the (block, kv head) tile; the tile starts at tile * kTileElems in either pool.
