@@ -35,10 +35,15 @@
  * Layouts (bf16 = IEEE binary16-brain, stored as 2 bytes)
  * --------------------------------------------------------
  *   q            bf16  [batch][num_q_heads][head_dim]
- *   k_cache      bf16  [num_blocks][num_kv_heads][block_size][head_dim]
- *                      token-major 4 KiB tile per (block, kv head)
+ *   k_cache      bf16  [num_blocks][num_kv_heads][head_dim / 8][block_size][8]
+ *                      4 KiB tile per (block, kv head) of 16-byte chunks of
+ *                      8 dims, chunk-major then token: element (token t,
+ *                      dim d) of a tile is at ((d / 8) * block_size + t) * 8 + d % 8
  *   v_cache      bf16  [num_blocks][num_kv_heads][head_dim][block_size]
- *                      dim-major 4 KiB tile per (block, kv head)
+ *                      dim-major 4 KiB tile per (block, kv head): element
+ *                      (token t, dim d) at d * block_size + t
+ *  (These are the key and value block layouts of the paged KV cache the
+ *  paper's serving system builds on.)
  *   block_table  int32 [batch][max_blocks_per_seq]
  *                      logical block j of sequence b -> physical block
  *   seq_lens     int32 [batch]  tokens in the cache, current token included
@@ -136,9 +141,9 @@ const char* bana_last_error(void);
  * Test hook for the address generator the attention kernel uses: for every
  * sequence b, kv head g and logical token t < max_blocks_per_seq * 16,
  *   rows_out[b][g][t] = (block_table[b][t / 16] * num_kv_heads + g) * 16 + t % 16
- * (the K row the partial kernel reads for that token; V is read from the
- * same (block, kv head) tile) when kv_range_begin[b] <= t < kv_range_end[b],
- * and -1 otherwise.  rows_out: int64 [batch][num_kv_heads][max_blocks_per_seq * 16].
+ * (the pool-wide (tile, slot) index whose key and value the partial kernel
+ * reads for that token) when kv_range_begin[b] <= t < kv_range_end[b], and
+ * -1 otherwise.  rows_out: int64 [batch][num_kv_heads][max_blocks_per_seq * 16].
  */
 bana_status bana_debug_kv_rows(const bana_dims* d, const int32_t* block_table, const int32_t* kv_range_begin,
                                const int32_t* kv_range_end, int64_t* rows_out, void* stream);

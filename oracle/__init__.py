@@ -81,8 +81,8 @@ def partial(q, k_cache, v_cache, block_table, seq_lens, kv_begin, kv_end,
     kv_begin = _c(kv_begin, np.int32)
     kv_end = _c(kv_end, np.int32)
     B, Hq, D = q.shape
-    nb, Hkv, bs, D2 = k_cache.shape
-    assert D2 == D and v_cache.shape == (nb, Hkv, D, bs)
+    nb, Hkv, nchunk, bs, x = k_cache.shape
+    assert nchunk * x == D and x == 8 and v_cache.shape == (nb, Hkv, D, bs)
     sel = None if seqs is None else _c(np.asarray(seqs), np.int32)
     n = B if sel is None else len(sel)
     out = np.zeros((n, Hq, D), dtype=np.float64)

@@ -28,7 +28,7 @@ def attention(q, k_cache, v_cache, block_table, seq_lens, ranges, b: int, h: int
     G = Hq // num_kv_heads
     g = h // G
     D = len(q[b][h])
-    bs = len(k_cache[0][0])
+    bs = len(v_cache[0][0][0])
     qv = [_bf16(x) for x in q[b][h]]
     num = [0.0] * D
     l = 0.0
@@ -36,10 +36,10 @@ def attention(q, k_cache, v_cache, block_table, seq_lens, ranges, b: int, h: int
         for t in range(t0, t1):
             blk = int(block_table[b][t // bs])
             slot = t % bs
-            kr = k_cache[blk][g][slot]
+            kt = k_cache[blk][g]  # [D/8][bs][8]
             s = 0.0
             for d in range(D):
-                s += qv[d] * _bf16(kr[d])
+                s += qv[d] * _bf16(kt[d // 8][slot][d % 8])
             a = math.exp(s)
             l += a
             vt = v_cache[blk][g]

@@ -29,7 +29,8 @@
  * Data (interface contract; bf16 values are uint16 bit patterns, widened
  * exactly to double):
  *   q            [B][Hq][D]
- *   k_cache      [num_blocks][Hkv][bs][D]   token-major tile per (block, kv-head)
+ *   k_cache      [num_blocks][Hkv][D/8][bs][8]  per (block, kv-head) tile: 16-byte chunks of 8 dims,
+ *                                              chunk-major, then token
  *   v_cache      [num_blocks][Hkv][D][bs]   dim-major tile per (block, kv-head)
  *   block_table  [B][max_blocks_per_seq]    logical block -> physical block
  *   query head h reads kv head g = h / (Hq / Hkv).
@@ -80,7 +81,8 @@ int oracle_partial(int B, int Hq, int Hkv, int D, int bs, int max_blocks, int64_
                    const int32_t* block_table, const int32_t* seq_lens,
                    const int32_t* kv_begin, const int32_t* kv_end,
                    const int32_t* seqs, int n_seqs, double* out, double* lse, int nthreads) {
-  if (B <= 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || bs <= 0 || max_blocks <= 0 || Hq % Hkv != 0) return -1;
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || D <= 0 || D % 8 != 0 || bs <= 0 || max_blocks <= 0 || Hq % Hkv != 0)
+    return -1;
   if (seqs == NULL) n_seqs = B;
   const int G = Hq / Hkv;
   for (int i = 0; i < n_seqs; ++i) {
@@ -121,9 +123,10 @@ int oracle_partial(int B, int Hq, int Hkv, int D, int bs, int max_blocks, int64_
       double m = -INFINITY;
       for (int t = t0; t < t1; ++t) {
         int64_t blk = phys_block(block_table, max_blocks, num_blocks, bs, b, t);
-        const uint16_t* kr = k_cache + ((blk * Hkv + g) * bs + (t % bs)) * (int64_t)D;
+        const uint16_t* kt = k_cache + (blk * Hkv + g) * (int64_t)D * bs;
+        const int slot = t % bs;
         double acc = 0.0;
-        for (int d = 0; d < D; ++d) acc += bf16_to_f64(qv[d]) * bf16_to_f64(kr[d]);
+        for (int d = 0; d < D; ++d) acc += bf16_to_f64(qv[d]) * bf16_to_f64(kt[((d / 8) * bs + slot) * 8 + d % 8]);
         s[t - t0] = acc;
         if (acc > m) m = acc;
       }
@@ -184,10 +187,10 @@ int oracle_merge(int n_parts, int64_t rows, int D, const double* outs, const dou
 
 /*
  * Address generator written from the layout contract: for every sequence b,
- * kv head g and logical token t of the table's span, the index of the K row
- * the attention must read, ((blk * Hkv + g) * bs + t % bs) with
- * blk = block_table[b][t / bs], or -1 when t lies outside [kv_begin[b],
- * kv_end[b]).  rows is [B][Hkv][max_blocks * bs].
+ * kv head g and logical token t of the table's span, the (tile, slot) index
+ * ((blk * Hkv + g) * bs + t % bs) of the key and value the attention must
+ * read, with blk = block_table[b][t / bs], or -1 when t lies outside
+ * [kv_begin[b], kv_end[b]).  rows is [B][Hkv][max_blocks * bs].
  */
 int oracle_kv_rows(int B, int Hkv, int bs, int max_blocks, int64_t num_blocks, const int32_t* block_table,
                    const int32_t* kv_begin, const int32_t* kv_end, int64_t* rows) {

@@ -114,7 +114,7 @@ def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape=None):
 def dims_for(q: torch.Tensor, k_cache: torch.Tensor, block_table: torch.Tensor, max_range_tokens: int = 0,
              waves_hint: int = 0, chunks_hint: int = 0) -> bana_dims:
     B, Hq, D = q.shape
-    nb, Hkv, bs, D2 = k_cache.shape
+    nb, Hkv, _, bs, _ = k_cache.shape
     return bana_dims(B, Hq, Hkv, D, bs, block_table.shape[1], nb, max_range_tokens, waves_hint, chunks_hint, 0)
 
 
@@ -126,12 +126,12 @@ def bana_decode_attn_partial(q, k_cache, v_cache, block_table, seq_lens, kv_rang
                              out_partial, lse, workspace: Optional[torch.Tensor] = None, stream=None,
                              dims: Optional[bana_dims] = None, max_range_tokens: int = 0) -> None:
     """Partial attention of one partition; see ``bana_decode_attn_partial`` in include/bana.h."""
-    if q.dim() != 3 or k_cache.dim() != 4:
-        raise ValueError("q must be [B, Hq, D] and k_cache [num_blocks, Hkv, block_size, D]")
+    if q.dim() != 3 or k_cache.dim() != 5:
+        raise ValueError("q must be [B, Hq, D] and k_cache [num_blocks, Hkv, D / 8, block_size, 8]")
     B, Hq, D = q.shape
-    nb, Hkv, bs, _ = k_cache.shape
+    nb, Hkv, _, bs, _ = k_cache.shape
     _need(q, "q", torch.bfloat16)
-    _need(k_cache, "k_cache", torch.bfloat16, (nb, Hkv, bs, D))
+    _need(k_cache, "k_cache", torch.bfloat16, (nb, Hkv, D // 8, bs, 8))
     _need(v_cache, "v_cache", torch.bfloat16, (nb, Hkv, D, bs))
     _need(block_table, "block_table", torch.int32)
     if block_table.dim() != 2 or block_table.shape[0] != B:

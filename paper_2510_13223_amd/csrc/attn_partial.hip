@@ -17,9 +17,10 @@
 //
 // One KV block (16 tokens x 128 dims for one kv head) per wavefront step:
 //   scores  S^T[16 tok x 16 col] = K[16 tok x 128] . Q^T[128 x 16 col]
-//           4 x v_mfma_f32_16x16x32_bf16, A = K rows straight from HBM
-//           (lane = token row, 16-byte loads), B = Q of the G heads of the
-//           group (columns >= G are zero).  bf16 x bf16 products are exact in
+//           4 x v_mfma_f32_16x16x32_bf16, A = K straight from HBM (lane =
+//           token row; the chunked K tile makes each 16-byte-per-lane load
+//           one contiguous 1 KiB), B = Q of the G heads of the group
+//           (columns >= G are zero).  bf16 x bf16 products are exact in
 //           fp32, accumulation is fp32.
 //   softmax running max per column (4 values per lane + two cross-lane
 //           shuffles), p = 2^((s - m) log2 e), rescale of the accumulator.
@@ -32,8 +33,10 @@
 //           part and a bf16 residual (two MFMAs per tile) so PV keeps ~16
 //           significant bits of P instead of bf16's 8.
 // K and V are read exactly once, so their loads carry the non-temporal hint
-// (streaming through the caches instead of allocating in them); on random
-// 4 KiB tiles this lifts sustained HBM read bandwidth by about a tenth.
+// (streaming through the caches instead of allocating in them).  With every
+// load instruction covering whole 128-byte lines (1 KiB for K, 512 bytes for
+// V) this lifts sustained HBM read bandwidth on random 4 KiB tiles by about
+// a tenth; loads that split lines across instructions do not gain.
 // Tokens of a partly covered block are selected out (score -inf, value 0),
 // never multiplied by zero, so NaN in unused slots cannot leak.
 #include <hip/hip_runtime.h>
@@ -81,12 +84,14 @@ __device__ __forceinline__ void split_bf16(float p, uint32_t& hi, uint32_t& lo) 
   lo = (ur + 0x7FFFu + ((ur >> 16) & 1u)) >> 16;
 }
 
-// K tile of one (block, kv head): lane (col, quad) takes token row col, dims 32kk + 8quad + [0, 8).
+// K tile of one (block, kv head), stored as 16 chunks of 8 dims x 16 tokens:
+// lane (col, quad) takes token row col, dims 32kk + 8quad + [0, 8), which is
+// chunk 4kk + quad, so instruction kk reads 1 KiB at lane * 16 bytes.
 __device__ __forceinline__ void load_k(u32x4 (&kr)[4], const uint16_t* __restrict__ k, int64_t tile, int col,
                                        int quad) {
-  const u32x4* src = reinterpret_cast<const u32x4*>(k + tile * kTileElems + k_row(0, col) * kHeadDim + 8 * quad);
+  const u32x4* src = reinterpret_cast<const u32x4*>(k + tile * kTileElems) + (quad * kBlockSize + col);
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) kr[kk] = __builtin_nontemporal_load(src + 4 * kk);
+  for (int kk = 0; kk < 4; ++kk) kr[kk] = __builtin_nontemporal_load(src + 4 * kBlockSize * kk);
 }
 
 // V tile (dim-major): lane (col, quad) takes dim 16dt + col, token slots 4quad + [0, 4).

@@ -1,9 +1,10 @@
-// debug_rows.hip -- export of the K rows the partial-attention kernel reads (test hook).
+// debug_rows.hip -- export of the (tile, slot) pairs the partial-attention kernel reads (test hook).
 //
 // Uses the same address helpers as the attention kernel: for each sequence b,
-// kv head g and logical token t of the table span, the K row of
-// (block_table[b][t / 16], g, slot t % 16) when t is inside [begin[b], end[b]),
-// else -1.  Entries of the table outside the covered blocks are never read.
+// kv head g and logical token t of the table span, the pool-wide slot index of
+// (tile (block_table[b][t / 16], g), slot t % 16) when t is inside
+// [begin[b], end[b]), else -1.  Table entries outside the covered blocks are
+// never read.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -26,7 +27,7 @@ __global__ __launch_bounds__(256) void debug_rows_kernel(const int32_t* __restri
   int64_t r = -1;
   if (t >= begin[b] && t < end[b]) {
     const int64_t tile = kv_tile(table_lookup(table, max_blocks, b, t / kBlockSize), g, Hkv);
-    r = k_row(tile, t % kBlockSize);
+    r = tile_slot(tile, t % kBlockSize);
   }
   rows[tid] = r;
 }

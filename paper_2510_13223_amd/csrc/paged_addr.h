@@ -1,9 +1,10 @@
 // paged_addr.h -- device-side address generation for the paged KV cache.
 //
 // Shared by the partial-attention kernel and the address-export test kernel
-// so that the rows the test sees are the rows the attention reads.  Layout:
-// K pool [num_blocks][Hkv][16][128] (token-major tile per (block, kv head)),
-// V pool [num_blocks][Hkv][128][16] (dim-major tile per (block, kv head)).
+// so that the slots the test sees are the slots the attention reads.  Layout
+// of the two pools, one 4 KiB tile per (block, kv head):
+// K pool [num_blocks][Hkv][128/8][16][8] (16-byte chunks of 8 dims, chunk-major, then token),
+// V pool [num_blocks][Hkv][128][16]      (dim-major).
 #pragma once
 
 #include <stdint.h>
@@ -28,7 +29,7 @@ __device__ __forceinline__ int64_t kv_tile(int32_t blk, int g, int num_kv_heads)
   return (int64_t)blk * num_kv_heads + g;
 }
 
-// K row (in units of kHeadDim elements) of slot `slot` of a tile.
-__device__ __forceinline__ int64_t k_row(int64_t tile, int slot) { return tile * kBlockSize + slot; }
+// Pool-wide index of slot `slot` of a tile (the token a (tile, slot) pair holds).
+__device__ __forceinline__ int64_t tile_slot(int64_t tile, int slot) { return tile * kBlockSize + slot; }
 
 }  // namespace bana

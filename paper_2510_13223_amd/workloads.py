@@ -8,7 +8,8 @@ What is generated (all host NumPy arrays; bf16 values are carried as their
 uint16 bit patterns because NumPy has no bfloat16):
 
 * ``q``            uint16 [B, Hq, D]                      bf16 query of the decode step
-* ``k_cache``      uint16 [num_blocks, Hkv, bs, D]         bf16 keys, token-major tile per (block, kv-head)
+* ``k_cache``      uint16 [num_blocks, Hkv, D/8, bs, 8]    bf16 keys; per (block, kv-head) tile, 16-byte
+                                                          chunks of 8 dims, chunk-major then token
 * ``v_cache``      uint16 [num_blocks, Hkv, D, bs]         bf16 values, dim-major tile per (block, kv-head)
 * ``block_table``  int32  [B, max_blocks_per_seq]          logical block -> physical block, -1 when unused
 * ``seq_lens``     int32  [B]                              tokens in the cache, current token included
@@ -46,6 +47,7 @@ import numpy as np
 
 HEAD_DIM = 128
 BLOCK_SIZE = 16
+K_CHUNK = 8  # bf16 elements per 16-byte key chunk
 BF16_NAN = np.uint16(0x7FC0)
 
 # Stream ids for independent PCG64 streams.
@@ -269,7 +271,7 @@ def build_workload(
 
     q = _gen_normal_bf16(seed, cfg_id, _S_Q, -1, (B, Hq, D), scale=q_scale)
 
-    k_cache = np.empty((num_blocks, Hkv, bs, D), dtype=np.uint16)
+    k_cache = np.empty((num_blocks, Hkv, D // K_CHUNK, bs, K_CHUNK), dtype=np.uint16)
     v_cache = np.empty((num_blocks, Hkv, D, bs), dtype=np.uint16)
     used = np.zeros(num_blocks, dtype=bool)
     used[phys_of_logical] = True
@@ -291,7 +293,7 @@ def build_workload(
             kk.transpose(0, 2, 1, 3)[tail] = BF16_NAN
             vv.transpose(0, 2, 1, 3)[tail] = BF16_NAN
         phys = phys_of_logical[lo:hi]
-        k_cache[phys] = kk
+        k_cache[phys] = kk.reshape(n, Hkv, bs, D // K_CHUNK, K_CHUNK).transpose(0, 1, 3, 2, 4)
         v_cache[phys] = vv.transpose(0, 1, 3, 2)
 
     nthr = threads or min(16, os.cpu_count() or 1)
@@ -349,6 +351,23 @@ def permute_physical(w: Workload, seed: int) -> Workload:
     v2[perm] = w.v_cache
     t2 = np.where(w.block_table >= 0, perm[np.maximum(w.block_table, 0)], -1).astype(np.int32)
     return dataclasses.replace(w, k_cache=k2, v_cache=v2, block_table=t2)
+
+
+def k_token_major(k_cache: np.ndarray) -> np.ndarray:
+    """Copy of a key pool as [num_blocks, Hkv, bs, D] (token-major rows)."""
+    nb, Hkv, nc, bs, x = k_cache.shape
+    return np.ascontiguousarray(k_cache.transpose(0, 1, 3, 2, 4)).reshape(nb, Hkv, bs, nc * x)
+
+
+def get_k_row(k_cache: np.ndarray, blk: int, g: int, slot: int) -> np.ndarray:
+    """The D bf16 key bits of slot `slot` of tile (blk, g)."""
+    return k_cache[blk, g, :, slot, :].reshape(-1).copy()
+
+
+def set_k_row(k_cache: np.ndarray, blk: int, g: int, slot: int, bits: np.ndarray) -> None:
+    """Overwrite the key of slot `slot` of tile (blk, g) with D bf16 bit patterns."""
+    nc, x = k_cache.shape[2], k_cache.shape[4]
+    k_cache[blk, g, :, slot, :] = np.asarray(bits, dtype=np.uint16).reshape(nc, x)
 
 
 def unsplit_ranges(w: Workload) -> Tuple[np.ndarray, np.ndarray]:

@@ -158,7 +158,7 @@ def _aim_dominant(w, part, seed):
             qf = W.bf16_bits_to_f32(w.q[b, g * G]).astype(np.float32)
             scale = np.float32(300.0 / float(qf @ qf))
             blk = w.block_table[b, t // 16]
-            w.k_cache[blk, g, t % 16, :] = W.f32_to_bf16_bits(qf * scale)
+            W.set_k_row(w.k_cache, blk, g, t % 16, W.f32_to_bf16_bits(qf * scale))
             chosen[(b, g)] = t
     return chosen
 

@@ -34,7 +34,7 @@ def _small(seed=0, B=2, Hq=4, Hkv=2, lens=(37, 64), ranges=None, q_scale=1.0 / m
 
 def _set_k_row(w, b, g, t, values_bits):
     blk = w.block_table[b, t // 16]
-    w.k_cache[blk, g, t % 16, :] = values_bits
+    W.set_k_row(w.k_cache, blk, g, t % 16, values_bits)
 
 
 def _v_row(w, b, g, t):
@@ -44,7 +44,7 @@ def _v_row(w, b, g, t):
 
 def _k_row(w, b, g, t):
     blk = w.block_table[b, t // 16]
-    return _f64(w.k_cache[blk, g, t % 16, :])
+    return _f64(W.get_k_row(w.k_cache, blk, g, t % 16))
 
 
 # --------------------------------------------------------------------------- inputs
@@ -79,7 +79,8 @@ def test_generator_deterministic_and_seeded():
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_generator_poison_and_coverage(seed):
     w = W.make_config("tiny", seed)
-    k = W.bf16_bits_to_f32(w.k_cache)
+    k = W.bf16_bits_to_f32(W.k_token_major(w.k_cache))  # [nb, Hkv, bs, D]
+    v = W.bf16_bits_to_f32(w.v_cache)  # [nb, Hkv, D, bs]
     used = np.zeros(w.num_blocks, bool)
     for b in range(w.batch):
         L = int(w.seq_lens[b])
@@ -90,12 +91,12 @@ def test_generator_poison_and_coverage(seed):
             assert not used[blk], "physical block used twice"
             used[blk] = True
             valid = min(16, L - 16 * j)
-            assert np.all(np.isfinite(k[blk, :, :valid, :]))
-            assert np.all(np.isnan(k[blk, :, valid:, :]))
+            assert np.all(np.isfinite(k[blk, :, :valid, :])) and np.all(np.isfinite(v[blk, :, :, :valid]))
+            assert np.all(np.isnan(k[blk, :, valid:, :])) and np.all(np.isnan(v[blk, :, :, valid:]))
         # partitions tile [0, L) in order
         assert w.kv_begin[0, b] == 0 and w.kv_end[-1, b] == L
         assert np.all(w.kv_end[:-1, b] == w.kv_begin[1:, b])
-    assert np.all(np.isnan(k[~used]))
+    assert np.all(np.isnan(k[~used])) and np.all(np.isnan(v[~used]))
     assert w.num_blocks == math.ceil(1.2 * used.sum())
 
 
@@ -138,7 +139,7 @@ def _dense_kv(w, b, g):
     L = int(w.seq_lens[b])
     t = np.arange(L)
     blk = w.block_table[b, t // 16]
-    k = _f64(w.k_cache[blk, g, t % 16, :])
+    k = _f64(W.k_token_major(w.k_cache)[blk, g, t % 16, :])
     v = _f64(w.v_cache[blk, g, :, t % 16])  # advanced indices first -> [L, D]
     return k, v
 
@@ -232,7 +233,7 @@ def test_equal_keys_give_mean_value():
     w = _small(seed=3, lens=(64, 40), ranges=[[(3, 61), (0, 40)]])
     for b in range(2):
         for g in range(2):
-            row = w.k_cache[w.block_table[b, 0], g, 0, :].copy()
+            row = W.get_k_row(w.k_cache, w.block_table[b, 0], g, 0)
             for t in range(int(w.kv_begin[0, b]), int(w.kv_end[0, b])):
                 _set_k_row(w, b, g, t, row)
     out, lse = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.kv_begin[0], w.kv_end[0])
@@ -298,7 +299,7 @@ def test_key_bias_shift_invariance():
     c = rng.integers(-16, 17, size=(2, 128)).astype(np.float32) / 8
     w2 = W.make_custom(8, 2, 4, 2, [48, 33], [[(0, 48), (0, 33)]], q_scale=1.0 / math.sqrt(128))
     w2.k_cache[...] = w.k_cache
-    shifted = W.bf16_bits_to_f32(w.k_cache) + c[None, :, None, :]
+    shifted = W.bf16_bits_to_f32(w.k_cache) + c.reshape(2, 16, 1, 8)[None]  # c[g, d] at [.., g, d // 8, ., d % 8]
     w2.k_cache[finite] = W.f32_to_bf16_bits(shifted)[finite]
     assert np.array_equal(W.bf16_bits_to_f32(w2.k_cache)[finite], shifted[finite])
     o1, l1 = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.kv_begin[0], w.kv_end[0])
@@ -325,10 +326,11 @@ def test_kv_rows_cover_each_token_once():
         allrows.append(rows)
     rows = np.stack(allrows)
     covered = rows[rows >= 0]
-    assert covered.size == len(np.unique(covered))  # no K row visited twice, across partitions too
+    assert covered.size == len(np.unique(covered))  # no (tile, slot) visited twice, across partitions too
     assert covered.size == int(w.seq_lens.sum()) * w.num_kv_heads  # union = [0, L_b) for every head
-    kflat = W.bf16_bits_to_f32(w.k_cache).reshape(-1, 128)
-    assert np.all(np.isfinite(kflat[covered]))
+    kflat = W.bf16_bits_to_f32(W.k_token_major(w.k_cache)).reshape(-1, 128)  # one row per (tile, slot)
+    vflat = W.bf16_bits_to_f32(w.v_cache).transpose(0, 1, 3, 2).reshape(-1, 128)
+    assert np.all(np.isfinite(kflat[covered])) and np.all(np.isfinite(vflat[covered]))
 
 
 def test_oracle_rejects_unmapped_tokens():
