@@ -85,6 +85,7 @@ typedef struct {
   int32_t waves_hint;         /* waves per (sequence, kv head, chunk): 1, 2, 4 or 8 */
   int32_t chunks_hint;        /* chunks a range may be split into (needs workspace) */
   int32_t reserved;           /* must be 0 */
+  int64_t total_range_tokens; /* sum over sequences of kv_range_end - kv_range_begin */
 } bana_dims;
 
 /*
@@ -121,7 +122,8 @@ size_t bana_decode_attn_workspace_bytes(const bana_dims* d);
  * lse_out = -inf;  otherwise M = max_J lses[p][r], w_p = exp(lses[p][r] - M),
  *   out[r]     = sum_J w_p out_partials[p][r] / sum_J w_p,
  *   lse_out[r] = M + ln sum_J w_p.
- * Rows of parts with lse = -inf are never read.  Summation runs in part order.
+ * Rows of parts with lse = -inf are never read.  Summation runs in an order
+ * fixed by n_parts alone, so results are deterministic.
  * Of d, only batch, num_q_heads and head_dim are read.
  *   out_partials fp32 [n_parts][batch][num_q_heads][head_dim]
  *   lses         fp32 [n_parts][batch][num_q_heads]

@@ -40,6 +40,7 @@ class bana_dims(ctypes.Structure):
         ("waves_hint", ctypes.c_int32),
         ("chunks_hint", ctypes.c_int32),
         ("reserved", ctypes.c_int32),
+        ("total_range_tokens", ctypes.c_int64),
     ]
 
 
@@ -81,9 +82,10 @@ def lib() -> ctypes.CDLL:
 
 
 def make_dims(batch: int, num_q_heads: int, num_kv_heads: int, max_blocks_per_seq: int, num_blocks: int,
-              max_range_tokens: int = 0, waves_hint: int = 0, chunks_hint: int = 0) -> bana_dims:
+              max_range_tokens: int = 0, waves_hint: int = 0, chunks_hint: int = 0,
+              total_range_tokens: int = 0) -> bana_dims:
     return bana_dims(batch, num_q_heads, num_kv_heads, HEAD_DIM, BLOCK_SIZE, max_blocks_per_seq, num_blocks,
-                     max_range_tokens, waves_hint, chunks_hint, 0)
+                     max_range_tokens, waves_hint, chunks_hint, 0, total_range_tokens)
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -112,10 +114,11 @@ def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape=None):
 
 
 def dims_for(q: torch.Tensor, k_cache: torch.Tensor, block_table: torch.Tensor, max_range_tokens: int = 0,
-             waves_hint: int = 0, chunks_hint: int = 0) -> bana_dims:
+             waves_hint: int = 0, chunks_hint: int = 0, total_range_tokens: int = 0) -> bana_dims:
     B, Hq, D = q.shape
     nb, Hkv, _, bs, _ = k_cache.shape
-    return bana_dims(B, Hq, Hkv, D, bs, block_table.shape[1], nb, max_range_tokens, waves_hint, chunks_hint, 0)
+    return bana_dims(B, Hq, Hkv, D, bs, block_table.shape[1], nb, max_range_tokens, waves_hint, chunks_hint, 0,
+                     total_range_tokens)
 
 
 def bana_decode_attn_workspace_bytes(dims: bana_dims) -> int:
@@ -164,7 +167,7 @@ def bana_merge_partials(out_partials, lses, out, lse_out: Optional[torch.Tensor]
     _need(out, "out", torch.float32, (B, Hq, D))
     if lse_out is not None:
         _need(lse_out, "lse_out", torch.float32, (B, Hq))
-    dims = bana_dims(B, Hq, 1, D, BLOCK_SIZE, 1, 1, 0, 0, 0, 0)
+    dims = bana_dims(B, Hq, 1, D, BLOCK_SIZE, 1, 1, 0, 0, 0, 0, 0)
     st = lib().bana_merge_partials(ctypes.byref(dims), _ptr(out_partials), _ptr(lses), n, _ptr(out), _ptr(lse_out),
                                    _stream(stream))
     if st != BANA_OK:
@@ -179,7 +182,7 @@ def bana_debug_kv_rows(block_table, kv_range_begin, kv_range_end, num_blocks: in
     _need(kv_range_begin, "kv_range_begin", torch.int32, (B,))
     _need(kv_range_end, "kv_range_end", torch.int32, (B,))
     _need(rows_out, "rows_out", torch.int64, (B, num_kv_heads, mb * BLOCK_SIZE))
-    dims = bana_dims(B, num_kv_heads, num_kv_heads, HEAD_DIM, BLOCK_SIZE, mb, num_blocks, 0, 0, 0, 0)
+    dims = bana_dims(B, num_kv_heads, num_kv_heads, HEAD_DIM, BLOCK_SIZE, mb, num_blocks, 0, 0, 0, 0, 0)
     st = lib().bana_debug_kv_rows(ctypes.byref(dims), _ptr(block_table), _ptr(kv_range_begin), _ptr(kv_range_end),
                                   _ptr(rows_out), _stream(stream))
     if st != BANA_OK:

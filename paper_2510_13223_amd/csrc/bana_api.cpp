@@ -22,7 +22,8 @@ constexpr int kHeadDim = 128;
 constexpr int kBlockSize = 16;
 constexpr int kMaxGroup = 16;           // query heads per kv head handled by one MFMA column tile
 constexpr int kTargetWaves = 256 * 16;  // 256 CUs x 16 resident wavefronts: one full dispatch round
-constexpr int kMaxBlocksPerWave = 64;   // longest run of blocks one wavefront should walk
+constexpr int kMinBlocksPerWave = 8;    // below this a wavefront spends more time starting than streaming
+constexpr int kMaxBlocksPerWave = 64;   // longest run of blocks one wavefront should walk (no hints)
 constexpr int kMaxChunks = 256;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -33,7 +34,8 @@ bana_status check_dims(const bana_dims* d) {
       d->max_blocks_per_seq <= 0 || d->num_blocks <= 0)
     return BANA_ERR_INVALID;
   if (d->num_q_heads % d->num_kv_heads != 0) return BANA_ERR_INVALID;
-  if (d->max_range_tokens < 0 || d->chunks_hint < 0 || d->reserved != 0) return BANA_ERR_INVALID;
+  if (d->max_range_tokens < 0 || d->chunks_hint < 0 || d->reserved != 0 || d->total_range_tokens < 0)
+    return BANA_ERR_INVALID;
   if (d->waves_hint != 0 && d->waves_hint != 1 && d->waves_hint != 2 && d->waves_hint != 4 && d->waves_hint != 8)
     return BANA_ERR_INVALID;
   if (d->head_dim != kHeadDim || d->block_size != kBlockSize) return BANA_ERR_UNSUPPORTED;
@@ -53,16 +55,20 @@ struct Plan {
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
-// Workgroups are (chunk, sequence, kv head).  Aim for one full round of
-// resident wavefronts over all (sequence, kv head) pairs, give every
-// wavefront at least a few blocks, and cut long ranges into chunks so no
-// wavefront walks more than kMaxBlocksPerWave blocks.
+// Workgroups are (chunk, sequence, kv head) with `waves` wavefronts each.
+// Aim for one full round of resident wavefronts: enough waves per
+// (sequence, kv head) pair to cover the GPU, and a per-wavefront share of
+// the call's blocks (from the total-tokens hint) that every range is cut
+// to, so a long range is spread over several workgroups instead of keeping
+// a few wavefronts busy after the rest have finished.  Short ranges keep
+// a single chunk.  Without hints the table width bounds the range length.
 Plan make_plan(const bana_dims* d) {
   const int64_t pairs = (int64_t)d->batch * d->num_kv_heads;
-  int64_t bound = d->max_blocks_per_seq;
-  if (d->max_range_tokens > 0) bound = std::min<int64_t>(bound, (d->max_range_tokens + kBlockSize - 1) / kBlockSize + 1);
+  int64_t bound = d->max_blocks_per_seq;  // blocks of the longest range
+  if (d->max_range_tokens > 0) bound = std::min<int64_t>(bound, (d->max_range_tokens + kBlockSize - 1) / kBlockSize);
+  bound = std::max<int64_t>(bound, 1);
   int64_t wpp = (kTargetWaves + pairs - 1) / pairs;
-  wpp = std::max<int64_t>(1, std::min<int64_t>(wpp, std::max<int64_t>(1, bound / 4)));
+  wpp = std::max<int64_t>(1, std::min<int64_t>(wpp, std::max<int64_t>(1, bound / kMinBlocksPerWave)));
   Plan p;
   if (d->waves_hint > 0)
     p.waves = d->waves_hint;
@@ -74,6 +80,22 @@ Plan make_plan(const bana_dims* d) {
   if (d->chunks_hint > 0) {
     p.nc = d->chunks_hint;
     p.cmin = 1;
+  } else if (d->total_range_tokens > 0) {
+    // (block, kv head) units of the call and the blocks per wavefront if they
+    // were spread evenly over one round of resident wavefronts.
+    const int64_t mean_blocks = std::max<int64_t>(1, d->total_range_tokens / (kBlockSize * (int64_t)d->batch) + 1);
+    const int64_t units = mean_blocks * pairs;
+    int64_t per_wave = (units + kTargetWaves - 1) / kTargetWaves;
+    // Rounding each range up to whole chunks adds at most one workgroup per
+    // (sequence, kv head) pair: leave that many slots free so the call still
+    // fits one dispatch round (a second, partly filled round would double
+    // the time of its workgroups).
+    const int64_t slots = kTargetWaves / p.waves;
+    if (pairs < slots) per_wave = std::max<int64_t>(per_wave, (units + p.waves * (slots - pairs) - 1) / (p.waves * (slots - pairs)));
+    per_wave = std::max<int64_t>(kMinBlocksPerWave, per_wave);
+    const int64_t chunk = per_wave * p.waves;
+    p.nc = ceil_div(bound, chunk);
+    p.cmin = (int)std::min<int64_t>(chunk, INT32_MAX);
   } else {
     p.nc = std::max(ceil_div(wpp, p.waves), ceil_div(bound, (int64_t)p.waves * kMaxBlocksPerWave));
     p.cmin = p.waves * 16;

@@ -6,10 +6,15 @@
 //   M = max_p lse_p,  w_p = exp(lse_p - M),
 //   out = sum_p w_p out_p / sum_p w_p,  lse_out = M + ln sum_p w_p,
 // skipping parts with lse_p = -inf (their out_p is never read); no live part
-// gives out = 0, lse_out = -inf.  Parts are summed in index order, so the
-// result is deterministic.  HBM-bound: one thread per 16-byte slice of a
-// 128-float row, 32 consecutive threads per row, so each part's row is read
-// with one fully coalesced 512-byte access.
+// gives out = 0, lse_out = -inf.
+//
+// HBM-bound.  32 consecutive threads cover one 128-float row (16 bytes each,
+// one coalesced 512-byte access per part).  With many parts per row (the
+// chunk partials of a long range, or many migrated partitions) the parts of
+// a row are spread over KP thread groups that load independently, so the
+// merge is not a chain of dependent loads; the KP partial sums are added in
+// group order through LDS.  The part-to-group assignment and every summation
+// order depend only on n_parts, so results are deterministic.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -21,32 +26,65 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+template <int KP>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ outs, const float* __restrict__ lses,
                                                     int n_parts, int64_t rows, float* __restrict__ out,
                                                     float* __restrict__ lse_out) {
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t row = tid >> 5;
-  const int d4 = (int)(tid & 31);
-  if (row >= rows) return;
+  constexpr int R = 256 / (32 * KP);  // rows per workgroup
+  __shared__ f32x4 sm_acc[KP > 1 ? R * KP * 32 : 1];
+  __shared__ float sm_w[KP > 1 ? R * KP : 1];
+  const int t = threadIdx.x;
+  const int d4 = t & 31;
+  const int k = (t >> 5) % KP;  // part group
+  const int rl = t / (32 * KP);
+  const int64_t row = (int64_t)blockIdx.x * R + rl;
+  const bool live = row < rows;
+
   float M = -INFINITY;
-  for (int p = 0; p < n_parts; ++p) M = fmaxf(M, lses[(int64_t)p * rows + row]);
+  if (live)
+    for (int p = 0; p < n_parts; ++p) M = fmaxf(M, lses[(int64_t)p * rows + row]);
+  float wsum = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (live && M != -INFINITY) {
+    for (int p = k; p < n_parts; p += KP) {
+      const float l = lses[(int64_t)p * rows + row];
+      if (l == -INFINITY) continue;
+      const float w = expf(l - M);
+      wsum += w;
+      acc += w * reinterpret_cast<const f32x4*>(outs + ((int64_t)p * rows + row) * 128)[d4];
+    }
+  }
+  if (KP > 1) {
+    sm_acc[(rl * KP + k) * 32 + d4] = acc;
+    if (d4 == 0) sm_w[rl * KP + k] = wsum;
+    __syncthreads();
+    if (k != 0) return;
+    acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    wsum = 0.f;
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+      acc += sm_acc[(rl * KP + j) * 32 + d4];
+      wsum += sm_w[rl * KP + j];
+    }
+  }
+  if (!live) return;
   f32x4* dst = reinterpret_cast<f32x4*>(out + row * 128) + d4;
   if (M == -INFINITY) {
     *dst = f32x4{0.f, 0.f, 0.f, 0.f};
     if (lse_out != nullptr && d4 == 0) lse_out[row] = -INFINITY;
     return;
   }
-  float wsum = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int p = 0; p < n_parts; ++p) {
-    const float l = lses[(int64_t)p * rows + row];
-    if (l == -INFINITY) continue;
-    const float w = expf(l - M);
-    wsum += w;
-    acc += w * reinterpret_cast<const f32x4*>(outs + ((int64_t)p * rows + row) * 128)[d4];
-  }
   *dst = acc * (1.0f / wsum);
   if (lse_out != nullptr && d4 == 0) lse_out[row] = M + logf(wsum);
+}
+
+template <int KP>
+hipError_t launch(const float* outs, const float* lses, int n_parts, int64_t rows, float* out, float* lse_out,
+                  hipStream_t stream) {
+  constexpr int R = 256 / (32 * KP);
+  const unsigned grid = (unsigned)((rows + R - 1) / R);
+  hipLaunchKernelGGL(merge_kernel<KP>, dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, rows, out, lse_out);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -54,10 +92,15 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ ou
 hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t rows, float* out, float* lse_out,
                         hipStream_t stream) {
   if (rows == 0) return hipSuccess;
-  const int64_t threads = rows * 32;
-  const unsigned grid = (unsigned)((threads + 255) / 256);
-  hipLaunchKernelGGL(merge_kernel, dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, rows, out, lse_out);
-  return hipGetLastError();
+  // With enough rows to fill the GPU, one thread group per row streams best.
+  // With few rows (long ranges of few sequences), spread a row's parts over
+  // up to 8 thread groups, at least 2 parts each.
+  if (rows < 4096) {
+    if (n_parts >= 16) return launch<8>(outs, lses, n_parts, rows, out, lse_out, stream);
+    if (n_parts >= 8) return launch<4>(outs, lses, n_parts, rows, out, lse_out, stream);
+    if (n_parts >= 4) return launch<2>(outs, lses, n_parts, rows, out, lse_out, stream);
+  }
+  return launch<1>(outs, lses, n_parts, rows, out, lse_out, stream);
 }
 
 }  // namespace bana

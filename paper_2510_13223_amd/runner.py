@@ -47,10 +47,11 @@ class DeviceWorkload:
 
         self.dims: List[bana.bana_dims] = []
         for p in range(P):
-            hint = int(np.max(w.kv_end[p].astype(np.int64) - w.kv_begin[p])) if range_hints else 0
+            lens = w.kv_end[p].astype(np.int64) - w.kv_begin[p]
             self.dims.append(bana.make_dims(B, Hq, w.num_kv_heads, w.max_blocks_per_seq, w.num_blocks,
-                                            max_range_tokens=max(hint, 0), waves_hint=waves_hint,
-                                            chunks_hint=chunks_hint))
+                                            max_range_tokens=int(lens.max()) if range_hints else 0,
+                                            waves_hint=waves_hint, chunks_hint=chunks_hint,
+                                            total_range_tokens=int(lens.sum()) if range_hints else 0))
         ws = max(bana.bana_decode_attn_workspace_bytes(d) for d in self.dims) if use_workspace else 0
         self.workspace: Optional[torch.Tensor] = (
             torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device) if ws > 0 else None)
@@ -76,7 +77,7 @@ class DeviceWorkload:
                 vp(self.seq_lens), vp(self.kv_begin[p]), vp(self.kv_end[p]), vp(self.out_partials[p]),
                 vp(self.lses[p]), ws_ptr, ws_bytes])
         B, Hq = self.w.batch, self.w.num_q_heads
-        self._merge_dims = bana.bana_dims(B, Hq, 1, bana.HEAD_DIM, bana.BLOCK_SIZE, 1, 1, 0, 0, 0, 0)
+        self._merge_dims = bana.bana_dims(B, Hq, 1, bana.HEAD_DIM, bana.BLOCK_SIZE, 1, 1, 0, 0, 0, 0, 0)
         self._merge_args = [ctypes.byref(self._merge_dims), vp(self.out_partials), vp(self.lses), self.w.n_parts,
                             vp(self.out), vp(self.lse_out)]
 
@@ -92,10 +93,13 @@ class DeviceWorkload:
 
     def step(self, stream: Optional[torch.cuda.Stream] = None) -> None:
         """All partitions, then the merge, on ``stream`` (default: torch's current stream)."""
-        h = ctypes.c_void_p((stream or torch.cuda.current_stream()).cuda_stream)
+        self.step_on(ctypes.c_void_p((stream or torch.cuda.current_stream()).cuda_stream))
+
+    def step_on(self, stream_handle: ctypes.c_void_p) -> None:
+        """All partitions, then the merge, on a raw HIP stream handle."""
         for p in range(self.w.n_parts):
-            self.partial(p, h)
-        self.merge(h)
+            self.partial(p, stream_handle)
+        self.merge(stream_handle)
 
     def results(self):
         """(out_partials, lses, out, lse_out) as host float32 arrays."""
