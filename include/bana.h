@@ -81,7 +81,7 @@ typedef struct {
   int64_t num_blocks;         /* physical blocks in each pool */
   /* Performance hints; 0 = let the library choose.  They never change
    * results beyond float rounding order and never limit coverage. */
-  int32_t max_range_tokens;   /* upper bound of kv_range_end - kv_range_begin */
+  int32_t max_range_tokens;   /* upper bound of kv_range_end - kv_range_begin over sequences */
   int32_t waves_hint;         /* waves per (sequence, kv head, chunk): 1, 2, 4 or 8 */
   int32_t chunks_hint;        /* chunks a range may be split into (needs workspace) */
   int32_t reserved;           /* must be 0 */
@@ -111,9 +111,32 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
                                      float* out_partial, float* lse, void* workspace, size_t workspace_bytes,
                                      void* stream);
 
-/* Bytes of workspace bana_decode_attn_partial can use for these dims (0 when
- * it would not split ranges); 0 for invalid dims. */
+/* Bytes of workspace bana_decode_attn_partial / bana_decode_attn_fused can
+ * use for these dims (0 when they would not split ranges); 0 for invalid dims. */
 size_t bana_decode_attn_workspace_bytes(const bana_dims* d);
+
+/*
+ * All partitions and their merge in one launch (Sec. 4.1(2): the partitions'
+ * attention followed by the final O = O^(1) + O^(2), fused).  Equals
+ * bana_decode_attn_partial on each of the n_parts ranges followed by
+ * bana_merge_partials, up to float rounding order:
+ *   out[b][h] / lse_out[b][h] = softmax attention of q[b][h] over the tokens
+ *   of all ranges [kv_range_begin[p][b], kv_range_end[p][b]), p < n_parts
+ * (a token covered by two ranges counts twice, as the merge of the two
+ * partials would count it).  No token at all gives out = 0, lse_out = -inf.
+ *   kv_range_begin / kv_range_end  int32 [n_parts][batch], 1 <= n_parts <= 64
+ *   out      fp32 [batch][num_q_heads][head_dim]
+ *   lse_out  fp32 [batch][num_q_heads]
+ * dims->max_range_tokens / total_range_tokens, when given, refer to the sum
+ * over a sequence's ranges.  Per-partition partials are not produced (use
+ * bana_decode_attn_partial for those).  Errors as for the partial call;
+ * n_parts > 64 gives BANA_ERR_UNSUPPORTED.
+ */
+bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* seq_lens,
+                                   const int32_t* kv_range_begin, const int32_t* kv_range_end, int32_t n_parts,
+                                   float* out, float* lse_out, void* workspace, size_t workspace_bytes,
+                                   void* stream);
 
 /*
  * Merge of n_parts partials (Sec. 4.1(2), final O = O^(1) + O^(2) with the

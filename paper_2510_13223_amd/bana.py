@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
     L.bana_decode_attn_partial.restype = ctypes.c_int
     L.bana_decode_attn_workspace_bytes.argtypes = [D]
     L.bana_decode_attn_workspace_bytes.restype = ctypes.c_size_t
+    L.bana_decode_attn_fused.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_int32, P, P, P, ctypes.c_size_t, P]
+    L.bana_decode_attn_fused.restype = ctypes.c_int
     L.bana_merge_partials.argtypes = [D, P, P, ctypes.c_int32, P, P, P]
     L.bana_merge_partials.restype = ctypes.c_int
     L.bana_status_string.argtypes = [ctypes.c_int]
@@ -155,6 +157,47 @@ def bana_decode_attn_partial(q, k_cache, v_cache, block_table, seq_lens, kv_rang
         _stream(stream))
     if st != BANA_OK:
         raise BanaError(st, "bana_decode_attn_partial")
+
+
+def _check_attn_inputs(q, k_cache, v_cache, block_table, seq_lens):
+    if q.dim() != 3 or k_cache.dim() != 5:
+        raise ValueError("q must be [B, Hq, D] and k_cache [num_blocks, Hkv, D / 8, block_size, 8]")
+    B, Hq, D = q.shape
+    nb, Hkv, _, bs, _ = k_cache.shape
+    _need(q, "q", torch.bfloat16)
+    _need(k_cache, "k_cache", torch.bfloat16, (nb, Hkv, D // 8, bs, 8))
+    _need(v_cache, "v_cache", torch.bfloat16, (nb, Hkv, D, bs))
+    _need(block_table, "block_table", torch.int32)
+    if block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError("block_table must be [B, max_blocks_per_seq]")
+    _need(seq_lens, "seq_lens", torch.int32, (B,))
+    return B, Hq, D
+
+
+def bana_decode_attn_fused(q, k_cache, v_cache, block_table, seq_lens, kv_range_begin, kv_range_end, out, lse_out,
+                           workspace: Optional[torch.Tensor] = None, stream=None,
+                           dims: Optional[bana_dims] = None) -> None:
+    """All partitions ``kv_range_begin/end [n_parts, B]`` and their merge in one launch; see include/bana.h."""
+    B, Hq, D = _check_attn_inputs(q, k_cache, v_cache, block_table, seq_lens)
+    if kv_range_begin.dim() != 2 or kv_range_begin.shape[1] != B:
+        raise ValueError("kv_range_begin must be [n_parts, B]")
+    n = kv_range_begin.shape[0]
+    _need(kv_range_begin, "kv_range_begin", torch.int32, (n, B))
+    _need(kv_range_end, "kv_range_end", torch.int32, (n, B))
+    _need(out, "out", torch.float32, (B, Hq, D))
+    _need(lse_out, "lse_out", torch.float32, (B, Hq))
+    ws_bytes = 0
+    if workspace is not None:
+        _need(workspace, "workspace", workspace.dtype)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    if dims is None:
+        dims = dims_for(q, k_cache, block_table)
+    st = lib().bana_decode_attn_fused(
+        ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens),
+        _ptr(kv_range_begin), _ptr(kv_range_end), n, _ptr(out), _ptr(lse_out), _ptr(workspace), ws_bytes,
+        _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_decode_attn_fused")
 
 
 def bana_merge_partials(out_partials, lses, out, lse_out: Optional[torch.Tensor] = None, stream=None) -> None:

@@ -1,15 +1,20 @@
 // attn_partial.hip -- partial attention of one KV partition over a paged cache (gfx950).
 //
-// Computes, per (sequence b, query head h) and over the logical tokens
-// [begin[b], end[b]) of one partition, the softmax-normalised partial output
-// and its log-sum-exp (paper Sec. 4.1(2): S = Q K^T, A = exp S, l = sum A,
-// O = A / l . V for one partition; the max-subtracted online form keeps the
-// same value in a finite range).
+// Computes, per (sequence b, query head h) and over the logical tokens of
+// the ranges [begin[p][b], end[p][b]) of n_parts partitions, the softmax-
+// normalised output and its log-sum-exp (paper Sec. 4.1(2): S = Q K^T,
+// A = exp S, l = sum A, O = A / l . V; the max-subtracted online form keeps
+// the same value in a finite range).  With one partition this is that
+// partition's partial; with several it is their merge (the online softmax
+// running over the partitions one after the other is the same log-sum-exp
+// algebra as the final O = O^(1) + O^(2)), computed in one launch.
 //
-// Work decomposition.  One workgroup per (chunk c, sequence b, kv head g),
-// linearised chunk-major so that every (b, g) has its first chunk in the
-// first wave of dispatch.  A workgroup of W wavefronts walks the KV blocks of
-// its chunk round-robin (block jr goes to wave jr % W); each wavefront keeps
+// Work decomposition.  The blocks of a sequence's ranges are concatenated
+// into one virtual block sequence.  One workgroup per (chunk c, sequence b,
+// kv head g), linearised chunk-major so that every (b, g) has its first
+// chunk in the first wave of dispatch.  A workgroup of W wavefronts walks the
+// virtual blocks of its chunk round-robin (block jr goes to wave jr % W),
+// mapping each to (range, logical block) with a segment cursor; each wavefront keeps
 // an online-softmax state for all G query heads of the kv head, and the W
 // states are combined through LDS at the end.  A range longer than one chunk
 // leaves one partial per chunk in caller workspace, merged by the merge
@@ -118,13 +123,25 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   const int G = a.G;
   const int hq0 = g * G;
 
-  const int t0 = a.begin[b];
-  const int t1 = a.end[b];
-  int nblk = 0, jfirst = 0;
-  if (t1 > t0) {
-    jfirst = t0 >> 4;
-    nblk = ((t1 - 1) >> 4) - jfirst + 1;
+  // The ranges ("segments") of this sequence: one per partition.  Lane p
+  // describes segment p; the segments' blocks are concatenated into one
+  // virtual block sequence [0, nblk) that the workgroup's chunks cut up.
+  int s_t0 = 0, s_t1 = 0, s_jfirst = 0, s_nblk = 0;
+  if (lane < a.n_parts) {
+    s_t0 = a.begin[(int64_t)lane * a.B + b];
+    s_t1 = a.end[(int64_t)lane * a.B + b];
+    if (s_t1 > s_t0) {
+      s_jfirst = s_t0 >> 4;
+      s_nblk = ((s_t1 - 1) >> 4) - s_jfirst + 1;
+    }
   }
+  int s_vend = s_nblk;  // inclusive prefix sum over segments
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(s_vend, off);
+    if (lane >= off) s_vend += y;
+  }
+  const int nblk = __builtin_amdgcn_readlane(s_vend, a.n_parts - 1);
   int per = (nblk + a.nc - 1) / a.nc;
   if (per < a.cmin) per = a.cmin;
   const int nch = nblk > 0 ? (nblk + per - 1) / per : 0;
@@ -172,7 +189,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     return s;
   };
   // Online-softmax update and value accumulation of one block.
-  auto update = [&](f32x4 s, u32x2 (&vr)[kDimTiles], const int j) {
+  auto update = [&](f32x4 s, u32x2 (&vr)[kDimTiles], const int j, const int t0, const int t1) {
     if (j * kBlockSize < t0 || j * kBlockSize + kBlockSize > t1) {  // partly covered block (wave-uniform)
       const int tok = j * kBlockSize + 4 * quad;
       const bool ok0 = tok + 0 >= t0 && tok + 0 < t1;
@@ -223,14 +240,40 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   // has consumed the current one, so about one block (8 KiB) per wave stays
   // in flight through the softmax and MFMA work.  Table entries are read two
   // blocks ahead with scalar loads.
-  int jr = jb0 + wave;
+  // Cursor over the segments (wave-uniform): the segment holding virtual
+  // block v, advanced monotonically with readlane from the segment lanes.
+  struct Seg {
+    int p, vstart, vend, jfirst, t0, t1;
+  };
+  auto seg_at = [&](int p) {
+    Seg sg;
+    sg.p = p;
+    sg.vend = __builtin_amdgcn_readlane(s_vend, p);
+    sg.vstart = sg.vend - __builtin_amdgcn_readlane(s_nblk, p);
+    sg.jfirst = __builtin_amdgcn_readlane(s_jfirst, p);
+    sg.t0 = __builtin_amdgcn_readlane(s_t0, p);
+    sg.t1 = __builtin_amdgcn_readlane(s_t1, p);
+    return sg;
+  };
+  auto seek = [&](Seg& sg, int v) {
+    while (v >= sg.vend && sg.p + 1 < a.n_parts) sg = seg_at(sg.p + 1);
+  };
+
+  int jr = jb0 + wave;  // virtual block index
   if (jr < jb1) {
-    const int jlast = jfirst + jb1 - 1;
-    int32_t blk_next = table_lookup(a.table, a.max_blocks, b, min(jfirst + jr + W, jlast));
+    const int vlast = jb1 - 1;
+    Seg cm = seg_at(0);  // segment of the block being computed
+    Seg ct = cm;         // segment of the block whose table entry is read
+    auto table_at = [&](int v) {
+      seek(ct, v);
+      return table_lookup(a.table, a.max_blocks, b, ct.jfirst + (v - ct.vstart));
+    };
+    const int32_t blk_first = table_at(jr);
+    int32_t blk_next = table_at(min(jr + W, vlast));
     u32x4 kr[4];
     u32x2 vr[kDimTiles];
     {
-      const int64_t tile = kv_tile(table_lookup(a.table, a.max_blocks, b, jfirst + jr), g, a.Hkv);
+      const int64_t tile = kv_tile(blk_first, g, a.Hkv);
       load_k(kr, a.k, tile, col, quad);
       load_v(vr, a.v, tile, col, quad);
     }
@@ -238,17 +281,18 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     // so the in-order memory counter lets each wait cover exactly the tile
     // it needs while the other one stays in flight.
     while (jr + W < jb1) {
-      const int j = jfirst + jr;
-      const int32_t blk_after = table_lookup(a.table, a.max_blocks, b, min(j + 2 * W, jlast));
+      const int32_t blk_after = table_at(min(jr + 2 * W, vlast));
       const int64_t tile_next = kv_tile(blk_next, g, a.Hkv);
       const f32x4 s = scores(kr);
       load_k(kr, a.k, tile_next, col, quad);
-      update(s, vr, j);
+      seek(cm, jr);
+      update(s, vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1);
       load_v(vr, a.v, tile_next, col, quad);
       jr += W;
       blk_next = blk_after;
     }
-    update(scores(kr), vr, jfirst + jr);
+    seek(cm, jr);
+    update(scores(kr), vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1);
   }
   // acc[dt][i] = unnormalised output for dim 16dt + 4quad + i, head col; the
   // per-lane lsum covers this lane's token rows only.

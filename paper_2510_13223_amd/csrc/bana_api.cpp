@@ -25,6 +25,7 @@ constexpr int kTargetWaves = 256 * 16;  // 256 CUs x 16 resident wavefronts: one
 constexpr int kMinBlocksPerWave = 8;    // below this a wavefront spends more time starting than streaming
 constexpr int kMaxBlocksPerWave = 64;   // longest run of blocks one wavefront should walk (no hints)
 constexpr int kMaxChunks = 256;
+constexpr int kMaxFusedParts = 64;  // one range per lane of the segment table
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -139,6 +140,57 @@ size_t bana_decode_attn_workspace_bytes(const bana_dims* d) {
   return workspace_for(d, make_plan(d).nc);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Shared by the per-partition and the fused entry points: n_parts ranges per
+// sequence ([n_parts][B] begin / end), result (merged over the ranges) into
+// out / lse.  Chunked plans leave chunk partials in the workspace and merge
+// them with the merge kernel.
+bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
+                          const int32_t* block_table, const int32_t* kv_range_begin, const int32_t* kv_range_end,
+                          int n_parts, float* out, float* lse, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  Plan plan = make_plan(d);
+  const size_t need = workspace_for(d, plan.nc);
+  if (plan.nc > 1 && (workspace == nullptr || workspace_bytes < need)) plan.nc = 1;
+
+  bana::PartialArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k_cache);
+  a.v = static_cast<const uint16_t*>(v_cache);
+  a.table = block_table;
+  a.begin = kv_range_begin;
+  a.end = kv_range_end;
+  a.n_parts = n_parts;
+  a.B = d->batch;
+  a.Hq = d->num_q_heads;
+  a.Hkv = d->num_kv_heads;
+  a.G = d->num_q_heads / d->num_kv_heads;
+  a.max_blocks = d->max_blocks_per_seq;
+  a.nc = plan.nc;
+  a.cmin = plan.cmin;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t rows = (int64_t)d->batch * d->num_q_heads;
+  if (plan.nc == 1) {
+    a.out = out;
+    a.lse = lse;
+    return device_status(bana::launch_partial_attn(a, plan.waves, s));
+  }
+  float* ws_out = static_cast<float*>(workspace);
+  float* ws_lse = ws_out + (size_t)plan.nc * rows * kHeadDim;
+  a.out = ws_out;
+  a.lse = ws_lse;
+  hipError_t e = bana::launch_partial_attn(a, plan.waves, s);
+  if (e != hipSuccess) return device_status(e);
+  return device_status(bana::launch_merge(ws_out, ws_lse, plan.nc, rows, out, lse, s));
+}
+
+}  // namespace
+
+extern "C" {
+
 bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
                                      const int32_t* block_table, const int32_t* seq_lens,
                                      const int32_t* kv_range_begin, const int32_t* kv_range_end,
@@ -152,39 +204,26 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out_partial) ||
       (workspace != nullptr && !aligned16(workspace)))
     return BANA_ERR_INVALID;
+  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, 1, out_partial, lse,
+                       workspace, workspace_bytes, stream);
+}
 
-  Plan plan = make_plan(d);
-  const size_t need = workspace_for(d, plan.nc);
-  if (plan.nc > 1 && (workspace == nullptr || workspace_bytes < need)) plan.nc = 1;
-
-  bana::PartialArgs a;
-  a.q = static_cast<const uint16_t*>(q);
-  a.k = static_cast<const uint16_t*>(k_cache);
-  a.v = static_cast<const uint16_t*>(v_cache);
-  a.table = block_table;
-  a.begin = kv_range_begin;
-  a.end = kv_range_end;
-  a.B = d->batch;
-  a.Hq = d->num_q_heads;
-  a.Hkv = d->num_kv_heads;
-  a.G = d->num_q_heads / d->num_kv_heads;
-  a.max_blocks = d->max_blocks_per_seq;
-  a.nc = plan.nc;
-  a.cmin = plan.cmin;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const int64_t rows = (int64_t)d->batch * d->num_q_heads;
-  if (plan.nc == 1) {
-    a.out = out_partial;
-    a.lse = lse;
-    return device_status(bana::launch_partial_attn(a, plan.waves, s));
-  }
-  float* ws_out = static_cast<float*>(workspace);
-  float* ws_lse = ws_out + (size_t)plan.nc * rows * kHeadDim;
-  a.out = ws_out;
-  a.lse = ws_lse;
-  hipError_t e = bana::launch_partial_attn(a, plan.waves, s);
-  if (e != hipSuccess) return device_status(e);
-  return device_status(bana::launch_merge(ws_out, ws_lse, plan.nc, rows, out_partial, lse, s));
+bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* seq_lens,
+                                   const int32_t* kv_range_begin, const int32_t* kv_range_end, int32_t n_parts,
+                                   float* out, float* lse_out, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !kv_range_begin || !kv_range_end || !out ||
+      !lse_out || n_parts < 1)
+    return BANA_ERR_INVALID;
+  if (n_parts > kMaxFusedParts) return BANA_ERR_UNSUPPORTED;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out) ||
+      (workspace != nullptr && !aligned16(workspace)))
+    return BANA_ERR_INVALID;
+  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts, out, lse_out,
+                       workspace, workspace_bytes, stream);
 }
 
 bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, const float* lses, int32_t n_parts,

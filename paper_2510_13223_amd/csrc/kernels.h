@@ -9,12 +9,13 @@ namespace bana {
 
 struct PartialArgs {
   const uint16_t* q;        // bf16 [B][Hq][128]
-  const uint16_t* k;        // bf16 [num_blocks][Hkv][16][128]
+  const uint16_t* k;        // bf16 [num_blocks][Hkv][128/8][16][8]
   const uint16_t* v;        // bf16 [num_blocks][Hkv][128][16]
   const int32_t* table;     // [B][max_blocks]
-  const int32_t* begin;     // [B]
-  const int32_t* end;       // [B]
-  float* out;               // nc == 1: final out_partial [B][Hq][128]; nc > 1: chunk partials [nc][B][Hq][128]
+  const int32_t* begin;     // [n_parts][B]
+  const int32_t* end;       // [n_parts][B]
+  int n_parts;              // ranges per sequence, 1..64
+  float* out;               // nc == 1: final output [B][Hq][128]; nc > 1: chunk partials [nc][B][Hq][128]
   float* lse;               // nc == 1: final lse [B][Hq];               nc > 1: chunk lses [nc][B][Hq]
   int B, Hq, Hkv, G, max_blocks;
   int nc;    // chunks per (sequence, kv head)

@@ -3,7 +3,8 @@
 Marshalling and orchestration only: uploads a ``workloads.Workload`` to
 device tensors once, pre-builds the ctypes argument lists, and issues the
 library calls (``bana_decode_attn_partial`` once per partition, then
-``bana_merge_partials``) on one stream.  No arithmetic happens here.
+``bana_merge_partials``; or the single ``bana_decode_attn_fused``) on one
+stream.  No arithmetic happens here.
 """
 
 from __future__ import annotations
@@ -52,7 +53,15 @@ class DeviceWorkload:
                                             max_range_tokens=int(lens.max()) if range_hints else 0,
                                             waves_hint=waves_hint, chunks_hint=chunks_hint,
                                             total_range_tokens=int(lens.sum()) if range_hints else 0))
-        ws = max(bana.bana_decode_attn_workspace_bytes(d) for d in self.dims) if use_workspace else 0
+        # The fused call sees each sequence's ranges as one concatenated range.
+        lens_all = (w.kv_end.astype(np.int64) - w.kv_begin).sum(axis=0)
+        self.fused_dims = bana.make_dims(B, Hq, w.num_kv_heads, w.max_blocks_per_seq, w.num_blocks,
+                                         max_range_tokens=int(lens_all.max()) if range_hints else 0,
+                                         waves_hint=waves_hint, chunks_hint=chunks_hint,
+                                         total_range_tokens=int(lens_all.sum()) if range_hints else 0)
+        self.fused_out = torch.empty((B, Hq, bana.HEAD_DIM), dtype=torch.float32, device=self.device)
+        self.fused_lse = torch.empty((B, Hq), dtype=torch.float32, device=self.device)
+        ws = max(bana.bana_decode_attn_workspace_bytes(d) for d in self.dims + [self.fused_dims]) if use_workspace else 0
         self.workspace: Optional[torch.Tensor] = (
             torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device) if ws > 0 else None)
         # Validate every argument once through the checked binding (this also runs the step once).
@@ -65,6 +74,9 @@ class DeviceWorkload:
                                           self.kv_begin[p], self.kv_end[p], self.out_partials[p], self.lses[p],
                                           workspace=self.workspace, stream=stream, dims=self.dims[p])
         bana.bana_merge_partials(self.out_partials, self.lses, self.out, self.lse_out, stream=stream)
+        bana.bana_decode_attn_fused(self.q, self.k_cache, self.v_cache, self.block_table, self.seq_lens,
+                                    self.kv_begin, self.kv_end, self.fused_out, self.fused_lse,
+                                    workspace=self.workspace, stream=stream, dims=self.fused_dims)
 
     def _prepare_fast_args(self) -> None:
         vp = lambda t: ctypes.c_void_p(t.data_ptr())
@@ -80,6 +92,9 @@ class DeviceWorkload:
         self._merge_dims = bana.bana_dims(B, Hq, 1, bana.HEAD_DIM, bana.BLOCK_SIZE, 1, 1, 0, 0, 0, 0, 0)
         self._merge_args = [ctypes.byref(self._merge_dims), vp(self.out_partials), vp(self.lses), self.w.n_parts,
                             vp(self.out), vp(self.lse_out)]
+        self._fused_args = [ctypes.byref(self.fused_dims), vp(self.q), vp(self.k_cache), vp(self.v_cache),
+                            vp(self.block_table), vp(self.seq_lens), vp(self.kv_begin), vp(self.kv_end),
+                            self.w.n_parts, vp(self.fused_out), vp(self.fused_lse), ws_ptr, ws_bytes]
 
     def partial(self, p: int, stream_handle: ctypes.c_void_p) -> None:
         st = bana.lib().bana_decode_attn_partial(*self._partial_args[p], stream_handle)
@@ -90,6 +105,12 @@ class DeviceWorkload:
         st = bana.lib().bana_merge_partials(*self._merge_args, stream_handle)
         if st != bana.BANA_OK:
             raise bana.BanaError(st, "bana_merge_partials")
+
+    def fused(self, stream_handle: ctypes.c_void_p) -> None:
+        """All partitions and their merge in one call (into fused_out / fused_lse)."""
+        st = bana.lib().bana_decode_attn_fused(*self._fused_args, stream_handle)
+        if st != bana.BANA_OK:
+            raise bana.BanaError(st, "bana_decode_attn_fused")
 
     def step(self, stream: Optional[torch.cuda.Stream] = None) -> None:
         """All partitions, then the merge, on ``stream`` (default: torch's current stream)."""
@@ -106,3 +127,8 @@ class DeviceWorkload:
         torch.cuda.synchronize(self.device)
         return (self.out_partials.cpu().numpy(), self.lses.cpu().numpy(), self.out.cpu().numpy(),
                 self.lse_out.cpu().numpy())
+
+    def fused_results(self):
+        """(out, lse_out) of the fused call as host float32 arrays."""
+        torch.cuda.synchronize(self.device)
+        return self.fused_out.cpu().numpy(), self.fused_lse.cpu().numpy()

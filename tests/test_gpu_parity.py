@@ -9,6 +9,7 @@ oracle's, zero keys give round(exp(lse)) == range length, and a dominant key
 returns its value row exactly.
 """
 
+import dataclasses
 import math
 import sys
 
@@ -88,7 +89,10 @@ def _full_parity(w, **kw):
     np.testing.assert_allclose(mo, uo, rtol=0, atol=1e-10)  # oracle's own merge == unsplit
     stats = _check_out(out, uo, f"{w.name} merged out")
     _check_lse(lse_out, ul, f"{w.name} merged lse")
-    _log(f"  merged max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
+    fo, fl = dw.fused_results()
+    fstats = _check_out(fo, mo, f"{w.name} fused out")
+    _check_lse(fl, ml, f"{w.name} fused lse")
+    _log(f"  merged max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e}; fused max-abs {fstats[0]:.2e} rel-L2 {fstats[1]:.2e}")
     return dw
 
 
@@ -182,13 +186,16 @@ def test_zero_keys_pin_coverage_counts():
         finite = np.isfinite(W.bf16_bits_to_f32(w.k_cache))
         w.k_cache[finite] = 0
         _log(f"[coverage] {name} {kw}")
-        op, lp, out, lse_out = DeviceWorkload(w, **kw).results()
+        dw = DeviceWorkload(w, **kw)
+        op, lp, out, lse_out = dw.results()
         n = (w.kv_end - w.kv_begin).astype(np.float64)[:, :, None].repeat(w.num_q_heads, 2)
         live = n > 0
         assert np.array_equal(np.rint(np.exp(lp[live].astype(np.float64))), n[live])
         assert np.all(np.isneginf(lp[~live]))
-        assert np.array_equal(np.rint(np.exp(lse_out.astype(np.float64))),
-                              w.seq_lens.astype(np.float64)[:, None].repeat(w.num_q_heads, 1))
+        L = w.seq_lens.astype(np.float64)[:, None].repeat(w.num_q_heads, 1)
+        assert np.array_equal(np.rint(np.exp(lse_out.astype(np.float64))), L)
+        fo, fl = dw.fused_results()
+        assert np.array_equal(np.rint(np.exp(fl.astype(np.float64))), L)
 
 
 def test_single_key_and_non_aligned_ranges():
@@ -227,6 +234,51 @@ def test_scaled_query_reading_llama_shape():
     ranges = [[(0, 179 * 16)] * 8, [(179 * 16, 4096)] * 8]
     w = W.make_custom(2, 8, 32, 8, lens, ranges, max_blocks_per_seq=256, q_scale=1 / math.sqrt(128))
     _full_parity(w)
+
+
+def _fused_vs_oracle(w, **kw):
+    dw = DeviceWorkload(w, **kw)
+    fo, fl = dw.fused_results()
+    ro, rl = oracle.workload_partials(w)
+    mo, ml = oracle.merge(ro, rl)
+    fin = np.isfinite(ml)
+    _check_out(fo[fin], mo[fin], "fused out")
+    assert np.all(fo[~fin] == 0.0)
+    _check_lse(fl, ml, "fused lse")
+
+
+def test_fused_overlapping_empty_and_many_ranges():
+    """Overlapping ranges count twice (as merging their partials would), empty ranges add nothing,
+    and up to 64 ranges per sequence are accepted."""
+    rng = np.random.default_rng(21)
+    lens = [700, 333, 1, 64, 0 + 17]
+    P = 64
+    ranges = []
+    for p in range(P):
+        row = []
+        for L in lens:
+            a, b = sorted(int(x) for x in rng.integers(0, L + 1, size=2))
+            row.append((a, b) if p % 7 else (a, a))  # every 7th range empty
+        ranges.append(row)
+    w = W.make_custom(5, len(lens), 8, 2, lens, ranges, q_scale=1 / math.sqrt(128))
+    _log("[fused] 64 overlapping ranges")
+    for kw in ({}, dict(waves_hint=8, chunks_hint=3), dict(waves_hint=1, chunks_hint=1)):
+        _fused_vs_oracle(w, **kw)
+
+
+def test_fused_dominant_key_and_all_empty():
+    w = W.make_config("tiny", 3)
+    chosen = _aim_dominant(w, 1, 11)
+    # tokens of partition 1 listed twice: the dominant key still wins alone
+    w2 = dataclasses.replace(w, kv_begin=np.concatenate([w.kv_begin, w.kv_begin[1:]]),
+                               kv_end=np.concatenate([w.kv_end, w.kv_end[1:]]))
+    fo, fl = DeviceWorkload(w2).fused_results()
+    for (b, g), t in chosen.items():
+        blk = w.block_table[b, t // 16]
+        assert np.array_equal(fo[b, g * w.group], W.bf16_bits_to_f32(w.v_cache[blk, g, :, t % 16]))
+    empty = dataclasses.replace(w, kv_begin=w.kv_end.copy())
+    fo, fl = DeviceWorkload(empty).fused_results()
+    assert np.all(fo == 0.0) and np.all(np.isneginf(fl))
 
 
 def test_merge_matches_oracle_merge():

@@ -103,6 +103,32 @@ def test_merge_rejects_bad_arguments(lib):
     assert lib.bana_debug_kv_rows(ctypes.byref(d), None, FAKE, FAKE, FAKE, None) == -1
 
 
+def test_fused_rejects_bad_arguments(lib):
+    d = _dims()
+
+    def fused(dd, n, ptrs=None):
+        p = ptrs or [FAKE] * 7
+        return lib.bana_decode_attn_fused(ctypes.byref(dd) if dd is not None else None, *p, n, FAKE, FAKE, None, 0,
+                                          None)
+
+    assert fused(d, 0) == -1
+    assert fused(d, -3) == -1
+    assert fused(d, 65) == -2
+    assert fused(None, 2) == -1
+    assert fused(_dims(head_dim=64), 2) == -2
+    for i in range(7):
+        ptrs = [FAKE] * 7
+        ptrs[i] = None
+        assert fused(d, 2, ptrs) == -1, i
+    assert lib.bana_decode_attn_fused(ctypes.byref(d), *[FAKE] * 7, 2, FAKE, None, None, 0, None) == -1
+
+
+def test_negative_total_hint_rejected(lib):
+    d = _dims()
+    d.total_range_tokens = -1
+    assert _partial(lib, d) == -1
+
+
 def test_workspace_sizing_follows_the_plan(lib):
     # 64 sequences x 8 kv heads fill the GPU with one chunk per (sequence, kv head): no workspace
     d = bana.make_dims(64, 32, 8, 256, 19661, max_range_tokens=2864)
