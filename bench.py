@@ -3,7 +3,9 @@
 
 One step = every partition's ``bana_decode_attn_partial`` call plus the
 ``bana_merge_partials`` call for one decode token of every sequence (one
-layer), on inputs already resident in HBM.  Default workload: the
+layer), on inputs already resident in HBM.  The same step through the fused
+entry point (``bana_decode_attn_fused``: all partitions and the merge in one
+launch) is timed as well and reported under ``fused_path``.  Default workload: the
 Llama-3-8B-shaped layer (batch 64, 32 query / 8 KV heads, head_dim 128,
 block 16, seq_len 4096, last 30 % of each sequence's blocks migrated ->
 2 partitions) over a 20 % oversized, randomly permuted block pool.
@@ -215,6 +217,18 @@ def main():
     stream.synchronize()
     torch.cuda.synchronize()
 
+    # Timed region 3: the same step through the fused entry point (every partition and the
+    # merge in one launch), K times, synchronised on both sides.
+    for _ in range(args.warmup):
+        dw.fused(h)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for _ in range(args.steps):
+        dw.fused(h)
+    torch.cuda.synchronize()
+    fused_ms = (time.perf_counter() - wall0) * 1e3 / args.steps
+    print(f"[bench] fused path: {fused_ms * 1e3:.1f} us/step", file=sys.stderr, flush=True)
+
     kv_bytes = w.kv_bytes()
     t_step = ms_per_step / 1e3
     # Partial-attention kernel: algorithmic bytes over its own launch durations.
@@ -244,6 +258,14 @@ def main():
         "tokens_per_s": round(w.batch / t_step, 1),
         "tokens_per_s_32_layers": round(w.batch / (32 * t_step), 1),
         "kv_bytes_per_step": kv_bytes,
+        "fused_path": {
+            "entry_point": "bana_decode_attn_fused",
+            "ms_per_step": round(fused_ms, 5),
+            "value": round(kv_bytes / (fused_ms / 1e3) / 1e9, 2),
+            "unit": "GB/s",
+            "frac_of_hbm_peak": round(kv_bytes / (fused_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+            "tokens_per_s": round(w.batch / (fused_ms / 1e3), 1),
+        },
         "partial_kernels_kv_gbs": round(partial_kv_gbs, 2),
         "roofline": {
             "bound": "hbm",

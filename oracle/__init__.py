@@ -42,9 +42,12 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(LIB_PATH):
+    # ORACLE_LIB points the tests at a deliberately broken copy of the oracle
+    # (tests/test_oracle_mutants.py checks that the pins reject each one).
+    path = os.environ.get("ORACLE_LIB", LIB_PATH)
+    if path == LIB_PATH and not os.path.exists(LIB_PATH):
         build()
-    lib = ctypes.CDLL(LIB_PATH)
+    lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     i32, i64 = ctypes.c_int, ctypes.c_int64
     lib.oracle_partial.argtypes = [i32, i32, i32, i32, i32, i32, i64, P, P, P, P, P, P, P, P, i32, P, P, i32]

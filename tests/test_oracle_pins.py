@@ -200,7 +200,7 @@ def test_merge_order_and_empty_parts():
     ro, rl = oracle.merge(outs[::-1].copy(), lses[::-1].copy())
     np.testing.assert_allclose(ro, mo, rtol=0, atol=1e-14)
     np.testing.assert_allclose(rl, ml, rtol=0, atol=1e-14)
-    junk = np.full_like(outs[:1], 12345.0)  # contents of an empty part are never read
+    junk = np.full_like(outs[:1], np.nan)  # contents of an empty part are never read
     eo = np.concatenate([junk, outs[:1], junk, outs[1:]])
     el = np.concatenate([np.full_like(lses[:1], -np.inf), lses[:1], np.full_like(lses[:1], -np.inf), lses[1:]])
     xo, xl = oracle.merge(eo, el)
