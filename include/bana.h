@@ -156,6 +156,31 @@ bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void
 bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, const float* lses, int32_t n_parts,
                                 float* out, float* lse_out, void* stream);
 
+/*
+ * KV-block migration (Sec. 4.1(2): the KV of the offloaded part moves to the
+ * cold device, T_attn ~ S_kv / B_net; Alg. 1's MigrateKVHeads): for every
+ * sequence b and logical block j in [blk_begin[b], blk_end[b]) (block
+ * units), copy the K and V tiles of all kv heads, bit for bit, from source
+ * block src_block_table[b][j] to destination block dst_block_table[b][j].
+ * After the call, attention over the migrated range through
+ * (dst pools, dst_block_table) equals attention through the source pools,
+ * bit for bit.
+ *   src pools     layouts as above, d->num_blocks blocks
+ *   dst pools     same layouts, dst_num_blocks blocks
+ *   tables        int32 [batch][max_blocks_per_seq]; only the entries of
+ *                 migrated blocks are read (the caller assigns destination
+ *                 blocks; they must not overlap blocks being read)
+ *   blk_begin/end int32 [batch], 0 <= begin <= end <= max_blocks_per_seq
+ * d->max_range_tokens, when given, is a hint for (blk_end - blk_begin) *
+ * block_size that sizes the launch (every block is copied regardless).
+ * Errors as for the other calls; more than 65535 sequences gives
+ * BANA_ERR_UNSUPPORTED.
+ */
+bana_status bana_migrate_kv_blocks(const bana_dims* d, const void* src_k_cache, const void* src_v_cache,
+                                   const int32_t* src_block_table, void* dst_k_cache, void* dst_v_cache,
+                                   const int32_t* dst_block_table, int64_t dst_num_blocks,
+                                   const int32_t* blk_begin, const int32_t* blk_end, void* stream);
+
 /* Static text for a status code. */
 const char* bana_status_string(bana_status s);
 

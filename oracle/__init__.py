@@ -143,3 +143,17 @@ def workload_unsplit(w, seqs=None, threads: int = 0):
     """Attention over [0, seq_len) of every (selected) sequence, no split."""
     return partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, np.zeros_like(w.seq_lens),
                    w.seq_lens, seqs=seqs, threads=threads)
+
+
+def migrate(src_k, src_v, src_table, dst_k, dst_v, dst_table, blk_begin, blk_end):
+    """KV-block migration written out (Sec. 4.1(2), the KV transfer of attention-level migration):
+    copies of the destination pools in which, for every sequence b and logical block j in
+    [blk_begin[b], blk_end[b]), block dst_table[b][j] holds the K/V tiles (all kv heads) of source
+    block src_table[b][j].  Returns (dst_k, dst_v)."""
+    dk = np.array(dst_k, copy=True)
+    dv = np.array(dst_v, copy=True)
+    for b in range(len(blk_begin)):
+        for j in range(int(blk_begin[b]), int(blk_end[b])):
+            dk[dst_table[b][j]] = src_k[src_table[b][j]]
+            dv[dst_table[b][j]] = src_v[src_table[b][j]]
+    return dk, dv

@@ -77,6 +77,8 @@ def lib() -> ctypes.CDLL:
     L.bana_status_string.restype = ctypes.c_char_p
     L.bana_last_error.argtypes = []
     L.bana_last_error.restype = ctypes.c_char_p
+    L.bana_migrate_kv_blocks.argtypes = [D, P, P, P, P, P, P, ctypes.c_int64, P, P, P]
+    L.bana_migrate_kv_blocks.restype = ctypes.c_int
     L.bana_debug_kv_rows.argtypes = [D, P, P, P, P, P]
     L.bana_debug_kv_rows.restype = ctypes.c_int
     _lib = L
@@ -215,6 +217,30 @@ def bana_merge_partials(out_partials, lses, out, lse_out: Optional[torch.Tensor]
                                    _stream(stream))
     if st != BANA_OK:
         raise BanaError(st, "bana_merge_partials")
+
+
+def bana_migrate_kv_blocks(src_k, src_v, src_table, dst_k, dst_v, dst_table, blk_begin, blk_end, stream=None,
+                           max_range_tokens: int = 0) -> None:
+    """Copy the K/V tiles of logical blocks [blk_begin, blk_end) between pools; see include/bana.h."""
+    if src_k.dim() != 5 or dst_k.dim() != 5:
+        raise ValueError("k pools must be [num_blocks, Hkv, D / 8, block_size, 8]")
+    nb, Hkv, _, bs, _ = src_k.shape
+    nbd = dst_k.shape[0]
+    B, mb = src_table.shape
+    _need(src_k, "src_k", torch.bfloat16, (nb, Hkv, HEAD_DIM // 8, bs, 8))
+    _need(src_v, "src_v", torch.bfloat16, (nb, Hkv, HEAD_DIM, bs))
+    _need(dst_k, "dst_k", torch.bfloat16, (nbd, Hkv, HEAD_DIM // 8, bs, 8))
+    _need(dst_v, "dst_v", torch.bfloat16, (nbd, Hkv, HEAD_DIM, bs))
+    _need(src_table, "src_table", torch.int32, (B, mb))
+    _need(dst_table, "dst_table", torch.int32, (B, mb))
+    _need(blk_begin, "blk_begin", torch.int32, (B,))
+    _need(blk_end, "blk_end", torch.int32, (B,))
+    dims = bana_dims(B, Hkv, Hkv, HEAD_DIM, bs, mb, nb, max_range_tokens, 0, 0, 0, 0)
+    st = lib().bana_migrate_kv_blocks(ctypes.byref(dims), _ptr(src_k), _ptr(src_v), _ptr(src_table), _ptr(dst_k),
+                                      _ptr(dst_v), _ptr(dst_table), nbd, _ptr(blk_begin), _ptr(blk_end),
+                                      _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_migrate_kv_blocks")
 
 
 def bana_debug_kv_rows(block_table, kv_range_begin, kv_range_end, num_blocks: int, num_kv_heads: int, rows_out,

@@ -238,6 +238,26 @@ bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, c
       bana::launch_merge(out_partials, lses, n_parts, rows, out, lse_out, static_cast<hipStream_t>(stream)));
 }
 
+bana_status bana_migrate_kv_blocks(const bana_dims* d, const void* src_k_cache, const void* src_v_cache,
+                                   const int32_t* src_block_table, void* dst_k_cache, void* dst_v_cache,
+                                   const int32_t* dst_block_table, int64_t dst_num_blocks,
+                                   const int32_t* blk_begin, const int32_t* blk_end, void* stream) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!src_k_cache || !src_v_cache || !src_block_table || !dst_k_cache || !dst_v_cache || !dst_block_table ||
+      !blk_begin || !blk_end || dst_num_blocks <= 0)
+    return BANA_ERR_INVALID;
+  if (!aligned16(src_k_cache) || !aligned16(src_v_cache) || !aligned16(dst_k_cache) || !aligned16(dst_v_cache))
+    return BANA_ERR_INVALID;
+  if (d->batch > 65535) return BANA_ERR_UNSUPPORTED;  // one grid row per sequence
+  // Blocks per sequence the grid must cover: the hint (in tokens) when given, else the table width.
+  int64_t maxb = d->max_blocks_per_seq;
+  if (d->max_range_tokens > 0) maxb = std::min<int64_t>(maxb, (d->max_range_tokens + kBlockSize - 1) / kBlockSize);
+  return device_status(bana::launch_migrate(src_k_cache, src_v_cache, src_block_table, dst_k_cache, dst_v_cache,
+                                            dst_block_table, blk_begin, blk_end, d->batch, d->max_blocks_per_seq,
+                                            (int)maxb, d->num_kv_heads, static_cast<hipStream_t>(stream)));
+}
+
 bana_status bana_debug_kv_rows(const bana_dims* d, const int32_t* block_table, const int32_t* kv_range_begin,
                                const int32_t* kv_range_end, int64_t* rows_out, void* stream) {
   const bana_status st = check_dims(d);

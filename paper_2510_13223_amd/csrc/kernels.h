@@ -29,6 +29,12 @@ hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stre
 hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t rows, float* out, float* lse_out,
                         hipStream_t stream);
 
+// Copy of the K/V tiles (all kv heads) of logical blocks [blk_begin[b], blk_end[b]) from the
+// src pool (src_table) to the dst pool (dst_table); grid covers max_migrated_blocks per sequence.
+hipError_t launch_migrate(const void* src_k, const void* src_v, const int32_t* src_table, void* dst_k, void* dst_v,
+                          const int32_t* dst_table, const int32_t* blk_begin, const int32_t* blk_end, int B,
+                          int max_blocks, int max_migrated_blocks, int Hkv, hipStream_t stream);
+
 // Address export for the tests (rows of the K pool visited per logical token).
 hipError_t launch_debug_rows(const int32_t* table, const int32_t* begin, const int32_t* end, int B, int Hkv,
                              int max_blocks, int64_t* rows, hipStream_t stream);

@@ -1,0 +1,82 @@
+// migrate.hip -- copy of the KV blocks of migrated ranges into another block pool (gfx950).
+//
+// The data movement behind attention-level migration (paper Sec. 4.1(2): the
+// KV of the offloaded part moves to the cold device, T_attn ~ S_kv / B_net;
+// Alg. 1's MigrateKVHeads step): for every sequence b and logical block j in
+// [blk_begin[b], blk_end[b]), the block's K and V tiles of all kv heads are
+// copied bit for bit from src block src_table[b][j] to dst block
+// dst_table[b][j].  In both pools a block's tiles for all kv heads are one
+// contiguous run (Hkv x 4 KiB for K, the same for V), so a block is two
+// contiguous copies.  A grid row per sequence whose workgroups stride over the
+// sequence's migrated blocks (the row width only sets parallelism); each
+// thread moves 16 bytes per step with non-temporal loads and stores (the data
+// is touched once).  HBM-bound: reads and writes Hkv x 8 KiB per block.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.h"
+#include "paged_addr.h"
+
+namespace bana {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;
+
+__global__ __launch_bounds__(kThreads) void migrate_kernel(const u32x4* __restrict__ src_k,
+                                                           const u32x4* __restrict__ src_v,
+                                                           const int32_t* __restrict__ src_table,
+                                                           u32x4* __restrict__ dst_k, u32x4* __restrict__ dst_v,
+                                                           const int32_t* __restrict__ dst_table,
+                                                           const int32_t* __restrict__ blk_begin,
+                                                           const int32_t* __restrict__ blk_end, int max_blocks,
+                                                           int Hkv) {
+  const int b = blockIdx.y;
+  const int jend = blk_end[b];
+  const int64_t n16 = (int64_t)Hkv * kTileElems / 8;  // 16-byte units per block and pool
+  // Workgroup x of the row takes blocks begin + x, begin + x + gridDim.x, ...
+  for (int j = blk_begin[b] + (int)blockIdx.x; j < jend; j += (int)gridDim.x) {
+    const int64_t sblk = table_lookup(src_table, max_blocks, b, j);
+    const int64_t dblk = table_lookup(dst_table, max_blocks, b, j);
+    const u32x4* sk = src_k + sblk * n16;
+    const u32x4* sv = src_v + sblk * n16;
+    u32x4* dk = dst_k + dblk * n16;
+    u32x4* dv = dst_v + dblk * n16;
+    for (int64_t i0 = threadIdx.x; i0 < n16; i0 += (int64_t)kThreads * kUnroll) {
+      u32x4 kx[kUnroll], vx[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int64_t i = i0 + (int64_t)u * kThreads;
+        if (i < n16) {
+          kx[u] = __builtin_nontemporal_load(sk + i);
+          vx[u] = __builtin_nontemporal_load(sv + i);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int64_t i = i0 + (int64_t)u * kThreads;
+        if (i < n16) {
+          __builtin_nontemporal_store(kx[u], dk + i);
+          __builtin_nontemporal_store(vx[u], dv + i);
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_migrate(const void* src_k, const void* src_v, const int32_t* src_table, void* dst_k, void* dst_v,
+                          const int32_t* dst_table, const int32_t* blk_begin, const int32_t* blk_end, int B,
+                          int max_blocks, int max_migrated_blocks, int Hkv, hipStream_t stream) {
+  if (max_migrated_blocks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(migrate_kernel, dim3((unsigned)max_migrated_blocks, (unsigned)B), dim3(kThreads), 0, stream,
+                     static_cast<const u32x4*>(src_k), static_cast<const u32x4*>(src_v), src_table,
+                     static_cast<u32x4*>(dst_k), static_cast<u32x4*>(dst_v), dst_table, blk_begin, blk_end,
+                     max_blocks, Hkv);
+  return hipGetLastError();
+}
+
+}  // namespace bana

@@ -373,3 +373,41 @@ def set_k_row(k_cache: np.ndarray, blk: int, g: int, slot: int, bits: np.ndarray
 def unsplit_ranges(w: Workload) -> Tuple[np.ndarray, np.ndarray]:
     """The single partition [0, seq_len) per sequence."""
     return np.zeros((1, w.batch), dtype=np.int32), w.seq_lens[None, :].astype(np.int32).copy()
+
+
+@dataclasses.dataclass
+class Migration:
+    """Destination pools and table for moving partition `part`'s blocks to another pool."""
+    dst_k: np.ndarray
+    dst_v: np.ndarray
+    dst_table: np.ndarray
+    blk_begin: np.ndarray
+    blk_end: np.ndarray
+
+    @property
+    def num_blocks(self) -> int:
+        return int(self.dst_k.shape[0])
+
+
+SENTINEL = np.uint16(0x7FC1)  # a NaN pattern distinct from the generator's poison
+
+
+def make_migration(w: Workload, part: int, seed: int = 0, pool_factor: float = 1.2) -> Migration:
+    """Blocks overlapping partition `part` of every sequence, each given a random block of a new
+    pool (pre-filled with a sentinel NaN pattern); other table entries are -1."""
+    t0 = w.kv_begin[part].astype(np.int64)
+    t1 = w.kv_end[part].astype(np.int64)
+    begin = np.where(t1 > t0, t0 // BLOCK_SIZE, 0).astype(np.int32)
+    end = np.where(t1 > t0, (t1 + BLOCK_SIZE - 1) // BLOCK_SIZE, 0).astype(np.int32)
+    n = int(np.sum(end - begin))
+    nb = max(1, int(math.ceil(pool_factor * n)))
+    perm = _rng(seed, 2000, _S_PERM).permutation(nb)
+    table = np.full_like(w.block_table, -1)
+    pos = 0
+    for b in range(w.batch):
+        k = int(end[b] - begin[b])
+        table[b, begin[b]:end[b]] = perm[pos:pos + k]
+        pos += k
+    dk = np.full((nb,) + w.k_cache.shape[1:], SENTINEL, dtype=np.uint16)
+    dv = np.full((nb,) + w.v_cache.shape[1:], SENTINEL, dtype=np.uint16)
+    return Migration(dk, dv, table, begin, end)

@@ -316,3 +316,36 @@ def test_non_default_stream_and_binding_checks():
     with pytest.raises(TypeError):
         bana.bana_decode_attn_partial(dw.q.float(), dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens,
                                       dw.kv_begin[0], dw.kv_end[0], dw.out_partials[0], dw.lses[0])
+
+
+@pytest.mark.parametrize("name,part", [("tiny", 0), ("tiny", 1), ("llama3_8b", 1), ("mixed", 1)])
+def test_migration_bit_exact_and_attention_unchanged(name, part):
+    """bana_migrate_kv_blocks equals the oracle's block copy bit for bit, leaves other destination
+    blocks untouched, and attention over the migrated partition is bit-identical afterwards."""
+    w = _workload(name)
+    m = W.make_migration(w, part, seed=4)
+    _log(f"[migrate] {name} part {part}: {int(np.sum(m.blk_end - m.blk_begin))} blocks")
+    dw = DeviceWorkload(w)
+    dk = torch.from_numpy(m.dst_k.view(np.int16)).view(torch.bfloat16).cuda()
+    dv = torch.from_numpy(m.dst_v.view(np.int16)).view(torch.bfloat16).cuda()
+    dt = torch.from_numpy(m.dst_table).cuda()
+    bb = torch.from_numpy(m.blk_begin).cuda()
+    be = torch.from_numpy(m.blk_end).cuda()
+    bana.bana_migrate_kv_blocks(dw.k_cache, dw.v_cache, dw.block_table, dk, dv, dt, bb, be)
+    ek, ev = oracle.migrate(w.k_cache, w.v_cache, w.block_table, m.dst_k, m.dst_v, m.dst_table, m.blk_begin,
+                            m.blk_end)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(dk.cpu().view(torch.int16).numpy().view(np.uint16), ek)
+    np.testing.assert_array_equal(dv.cpu().view(torch.int16).numpy().view(np.uint16), ev)
+    # attention over the partition through the destination pool and table
+    B, Hq = w.batch, w.num_q_heads
+    o1 = torch.empty((B, Hq, 128), dtype=torch.float32, device="cuda")
+    l1 = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+    d2 = bana.make_dims(B, Hq, w.num_kv_heads, w.max_blocks_per_seq, m.num_blocks,
+                        max_range_tokens=dw.dims[part].max_range_tokens,
+                        total_range_tokens=dw.dims[part].total_range_tokens)
+    bana.bana_decode_attn_partial(dw.q, dk, dv, dt, dw.seq_lens, dw.kv_begin[part], dw.kv_end[part], o1, l1,
+                                  workspace=dw.workspace, dims=d2)
+    op, lp, _, _ = dw.results()
+    assert np.array_equal(o1.cpu().numpy(), op[part], equal_nan=True)
+    assert np.array_equal(l1.cpu().numpy(), lp[part], equal_nan=True)

@@ -123,6 +123,23 @@ def test_fused_rejects_bad_arguments(lib):
     assert lib.bana_decode_attn_fused(ctypes.byref(d), *[FAKE] * 7, 2, FAKE, None, None, 0, None) == -1
 
 
+def test_migrate_rejects_bad_arguments(lib):
+    d = _dims()
+    args = [FAKE] * 6
+    assert lib.bana_migrate_kv_blocks(ctypes.byref(d), *args, 0, FAKE, FAKE, None) == -1
+    for i in range(6):
+        a = list(args)
+        a[i] = None
+        assert lib.bana_migrate_kv_blocks(ctypes.byref(d), *a, 10, FAKE, FAKE, None) == -1, i
+    for i in (0, 1, 3, 4):
+        a = list(args)
+        a[i] = ctypes.c_void_p(0x100008)
+        assert lib.bana_migrate_kv_blocks(ctypes.byref(d), *a, 10, FAKE, FAKE, None) == -1, i
+    assert lib.bana_migrate_kv_blocks(ctypes.byref(d), *args, 10, None, FAKE, None) == -1
+    assert lib.bana_migrate_kv_blocks(ctypes.byref(_dims(block_size=8)), *args, 10, FAKE, FAKE, None) == -2
+    assert lib.bana_migrate_kv_blocks(ctypes.byref(_dims(batch=70000)), *args, 10, FAKE, FAKE, None) == -2
+
+
 def test_negative_total_hint_rejected(lib):
     d = _dims()
     d.total_range_tokens = -1

@@ -339,3 +339,23 @@ def test_oracle_rejects_unmapped_tokens():
     bad[0, 1] = -1
     with pytest.raises(ValueError):
         oracle.partial(w.q, w.k_cache, w.v_cache, bad, w.seq_lens, w.kv_begin[1], w.kv_end[1])
+
+
+# --------------------------------------------------------------------------- KV-block migration
+
+@pytest.mark.parametrize("seed,part", [(0, 0), (1, 1), (2, 1)])
+def test_migrated_partition_attends_identically(seed, part):
+    """After moving a partition's blocks to another pool, attention over it through the new pool and
+    table is bit-identical to attention through the old ones; blocks not migrated stay untouched."""
+    w = W.make_config("tiny", seed)
+    m = W.make_migration(w, part, seed)
+    dk, dv = oracle.migrate(w.k_cache, w.v_cache, w.block_table, m.dst_k, m.dst_v, m.dst_table,
+                            m.blk_begin, m.blk_end)
+    a = oracle.partial(w.q, w.k_cache, w.v_cache, w.block_table, w.seq_lens, w.kv_begin[part], w.kv_end[part])
+    b = oracle.partial(w.q, dk, dv, m.dst_table, w.seq_lens, w.kv_begin[part], w.kv_end[part])
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    used = np.unique(m.dst_table[m.dst_table >= 0])
+    untouched = np.setdiff1d(np.arange(m.num_blocks), used)
+    assert untouched.size > 0 and np.all(dk[untouched] == W.SENTINEL) and np.all(dv[untouched] == W.SENTINEL)
+    assert used.size == int(np.sum(m.blk_end - m.blk_begin))
