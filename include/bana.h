@@ -111,8 +111,29 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
                                      float* out_partial, float* lse, void* workspace, size_t workspace_bytes,
                                      void* stream);
 
-/* Bytes of workspace bana_decode_attn_partial / bana_decode_attn_fused can
- * use for these dims (0 when they would not split ranges); 0 for invalid dims. */
+/*
+ * Head-split partition: the literal reading of Sec. 4.1(2), where the KV
+ * cache is split "along the attention head dimension" -- KV_1 keeps some kv
+ * heads on the hot device, KV_2 the others on the cold device.  Computes, for
+ * the kv heads [kv_head_begin, kv_head_end) only, exactly what
+ * bana_decode_attn_partial computes for them over the same range, bit for bit
+ * (the launch plan is taken from the full dims), and writes only the rows of
+ * their query heads (h with h / G in the kv-head range) of out / lse; other
+ * rows are left untouched.  With head partitions the "merge" is the
+ * concatenation of rows: calls over complementary kv-head ranges give the
+ * full result.  An empty kv-head range does nothing.  Other arguments and
+ * errors as for bana_decode_attn_partial; a kv-head range outside
+ * [0, num_kv_heads] gives BANA_ERR_INVALID.
+ */
+bana_status bana_decode_attn_heads(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* seq_lens,
+                                   const int32_t* kv_range_begin, const int32_t* kv_range_end,
+                                   int32_t kv_head_begin, int32_t kv_head_end, float* out, float* lse,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace bana_decode_attn_partial / bana_decode_attn_fused /
+ * bana_decode_attn_heads can use for these dims (0 when they would not split
+ * ranges); 0 for invalid dims. */
 size_t bana_decode_attn_workspace_bytes(const bana_dims* d);
 
 /*

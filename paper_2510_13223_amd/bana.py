@@ -77,6 +77,9 @@ def lib() -> ctypes.CDLL:
     L.bana_status_string.restype = ctypes.c_char_p
     L.bana_last_error.argtypes = []
     L.bana_last_error.restype = ctypes.c_char_p
+    L.bana_decode_attn_heads.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, P,
+                                         ctypes.c_size_t, P]
+    L.bana_decode_attn_heads.restype = ctypes.c_int
     L.bana_migrate_kv_blocks.argtypes = [D, P, P, P, P, P, P, ctypes.c_int64, P, P, P]
     L.bana_migrate_kv_blocks.restype = ctypes.c_int
     L.bana_debug_kv_rows.argtypes = [D, P, P, P, P, P]
@@ -200,6 +203,29 @@ def bana_decode_attn_fused(q, k_cache, v_cache, block_table, seq_lens, kv_range_
         _stream(stream))
     if st != BANA_OK:
         raise BanaError(st, "bana_decode_attn_fused")
+
+
+def bana_decode_attn_heads(q, k_cache, v_cache, block_table, seq_lens, kv_range_begin, kv_range_end,
+                           kv_head_begin: int, kv_head_end: int, out, lse, workspace: Optional[torch.Tensor] = None,
+                           stream=None, dims: Optional[bana_dims] = None) -> None:
+    """Head-split partition: the kv heads [kv_head_begin, kv_head_end) only; see include/bana.h."""
+    B, Hq, D = _check_attn_inputs(q, k_cache, v_cache, block_table, seq_lens)
+    _need(kv_range_begin, "kv_range_begin", torch.int32, (B,))
+    _need(kv_range_end, "kv_range_end", torch.int32, (B,))
+    _need(out, "out", torch.float32, (B, Hq, D))
+    _need(lse, "lse", torch.float32, (B, Hq))
+    ws_bytes = 0
+    if workspace is not None:
+        _need(workspace, "workspace", workspace.dtype)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    if dims is None:
+        dims = dims_for(q, k_cache, block_table)
+    st = lib().bana_decode_attn_heads(
+        ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens),
+        _ptr(kv_range_begin), _ptr(kv_range_end), int(kv_head_begin), int(kv_head_end), _ptr(out), _ptr(lse),
+        _ptr(workspace), ws_bytes, _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_decode_attn_heads")
 
 
 def bana_merge_partials(out_partials, lses, out, lse_out: Optional[torch.Tensor] = None, stream=None) -> None:

@@ -116,8 +116,8 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   const int quad = lane >> 4;
 
   int wg = blockIdx.x;
-  const int g = wg % a.Hkv;
-  wg /= a.Hkv;
+  const int g = a.g0 + wg % a.ng;
+  wg /= a.ng;
   const int b = wg % a.B;
   const int c = wg / a.B;
   const int G = a.G;
@@ -346,7 +346,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
 }  // namespace
 
 hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stream) {
-  const unsigned nwg = (unsigned)a.nc * (unsigned)a.B * (unsigned)a.Hkv;
+  const unsigned nwg = (unsigned)a.nc * (unsigned)a.B * (unsigned)a.ng;
   const size_t smem = waves > 1 ? sizeof(float) * (size_t)(32 * waves + waves * a.G * kRowPad) : 0;
   switch (waves) {
     case 1: hipLaunchKernelGGL(partial_attn_kernel<1>, dim3(nwg), dim3(64), smem, stream, a); break;

@@ -150,8 +150,8 @@ namespace {
 // them with the merge kernel.
 bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
                           const int32_t* block_table, const int32_t* kv_range_begin, const int32_t* kv_range_end,
-                          int n_parts, float* out, float* lse, void* workspace, size_t workspace_bytes,
-                          void* stream) {
+                          int n_parts, int g0, int ng, float* out, float* lse, void* workspace,
+                          size_t workspace_bytes, void* stream) {
   Plan plan = make_plan(d);
   const size_t need = workspace_for(d, plan.nc);
   if (plan.nc > 1 && (workspace == nullptr || workspace_bytes < need)) plan.nc = 1;
@@ -169,6 +169,8 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
   a.Hkv = d->num_kv_heads;
   a.G = d->num_q_heads / d->num_kv_heads;
   a.max_blocks = d->max_blocks_per_seq;
+  a.g0 = g0;
+  a.ng = ng;
   a.nc = plan.nc;
   a.cmin = plan.cmin;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -184,7 +186,8 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
   a.lse = ws_lse;
   hipError_t e = bana::launch_partial_attn(a, plan.waves, s);
   if (e != hipSuccess) return device_status(e);
-  return device_status(bana::launch_merge(ws_out, ws_lse, plan.nc, rows, out, lse, s));
+  return device_status(bana::launch_merge(ws_out, ws_lse, plan.nc, d->batch, d->num_q_heads, g0 * a.G, ng * a.G, out,
+                                          lse, s));
 }
 
 }  // namespace
@@ -204,8 +207,8 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out_partial) ||
       (workspace != nullptr && !aligned16(workspace)))
     return BANA_ERR_INVALID;
-  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, 1, out_partial, lse,
-                       workspace, workspace_bytes, stream);
+  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, 1, 0, d->num_kv_heads,
+                       out_partial, lse, workspace, workspace_bytes, stream);
 }
 
 bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
@@ -222,8 +225,27 @@ bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out) ||
       (workspace != nullptr && !aligned16(workspace)))
     return BANA_ERR_INVALID;
-  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts, out, lse_out,
-                       workspace, workspace_bytes, stream);
+  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts, 0,
+                       d->num_kv_heads, out, lse_out, workspace, workspace_bytes, stream);
+}
+
+bana_status bana_decode_attn_heads(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* seq_lens,
+                                   const int32_t* kv_range_begin, const int32_t* kv_range_end,
+                                   int32_t kv_head_begin, int32_t kv_head_end, float* out, float* lse,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !kv_range_begin || !kv_range_end || !out || !lse)
+    return BANA_ERR_INVALID;
+  if (kv_head_begin < 0 || kv_head_end > d->num_kv_heads || kv_head_begin > kv_head_end) return BANA_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out) ||
+      (workspace != nullptr && !aligned16(workspace)))
+    return BANA_ERR_INVALID;
+  if (kv_head_begin == kv_head_end) return BANA_OK;
+  // The plan comes from the full dims, so every head is computed exactly as by the full call.
+  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, 1, kv_head_begin,
+                       kv_head_end - kv_head_begin, out, lse, workspace, workspace_bytes, stream);
 }
 
 bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, const float* lses, int32_t n_parts,
@@ -233,9 +255,8 @@ bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, c
   if (d->head_dim != kHeadDim) return BANA_ERR_UNSUPPORTED;
   if (!out_partials || !lses || !out || n_parts < 1) return BANA_ERR_INVALID;
   if (!aligned16(out_partials) || !aligned16(out)) return BANA_ERR_INVALID;
-  const int64_t rows = (int64_t)d->batch * d->num_q_heads;
-  return device_status(
-      bana::launch_merge(out_partials, lses, n_parts, rows, out, lse_out, static_cast<hipStream_t>(stream)));
+  return device_status(bana::launch_merge(out_partials, lses, n_parts, d->batch, d->num_q_heads, 0, d->num_q_heads, out,
+                                          lse_out, static_cast<hipStream_t>(stream)));
 }
 
 bana_status bana_migrate_kv_blocks(const bana_dims* d, const void* src_k_cache, const void* src_v_cache,

@@ -18,6 +18,7 @@ struct PartialArgs {
   float* out;               // nc == 1: final output [B][Hq][128]; nc > 1: chunk partials [nc][B][Hq][128]
   float* lse;               // nc == 1: final lse [B][Hq];               nc > 1: chunk lses [nc][B][Hq]
   int B, Hq, Hkv, G, max_blocks;
+  int g0, ng;  // kv heads [g0, g0 + ng) of this launch
   int nc;    // chunks per (sequence, kv head)
   int cmin;  // minimum blocks per chunk
 };
@@ -25,9 +26,10 @@ struct PartialArgs {
 // Partial attention: one workgroup of `waves` wavefronts per (chunk, sequence, kv head).
 hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stream);
 
-// Log-sum-exp merge of n_parts partials over `rows` rows of 128 floats.
-hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t rows, float* out, float* lse_out,
-                        hipStream_t stream);
+// Log-sum-exp merge of n_parts partials over the rows (b, h) of B sequences x Hq heads restricted
+// to heads [h0, h0 + hn): partials are [n_parts][B][Hq][128] / [n_parts][B][Hq], outputs [B][Hq][128].
+hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn,
+                        float* out, float* lse_out, hipStream_t stream);
 
 // Copy of the K/V tiles (all kv heads) of logical blocks [blk_begin[b], blk_end[b]) from the
 // src pool (src_table) to the dst pool (dst_table); grid covers max_migrated_blocks per sequence.

@@ -28,8 +28,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <int KP>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ outs, const float* __restrict__ lses,
-                                                    int n_parts, int64_t rows, float* __restrict__ out,
-                                                    float* __restrict__ lse_out) {
+                                                    int n_parts, int64_t B, int Hq, int h0, int hn,
+                                                    float* __restrict__ out, float* __restrict__ lse_out) {
   constexpr int R = 256 / (32 * KP);  // rows per workgroup
   __shared__ f32x4 sm_acc[KP > 1 ? R * KP * 32 : 1];
   __shared__ float sm_w[KP > 1 ? R * KP : 1];
@@ -37,8 +37,10 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ ou
   const int d4 = t & 31;
   const int k = (t >> 5) % KP;  // part group
   const int rl = t / (32 * KP);
-  const int64_t row = (int64_t)blockIdx.x * R + rl;
-  const bool live = row < rows;
+  const int64_t r = (int64_t)blockIdx.x * R + rl;  // row among the B x hn merged rows
+  const int64_t rows = B * Hq;                      // row stride of one part
+  const bool live = r < B * hn;
+  const int64_t row = live ? (r / hn) * Hq + h0 + r % hn : 0;
 
   float M = -INFINITY;
   if (live)
@@ -79,28 +81,31 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ ou
 }
 
 template <int KP>
-hipError_t launch(const float* outs, const float* lses, int n_parts, int64_t rows, float* out, float* lse_out,
-                  hipStream_t stream) {
+hipError_t launch(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn, float* out,
+                  float* lse_out, hipStream_t stream) {
   constexpr int R = 256 / (32 * KP);
+  const int64_t rows = B * hn;
   const unsigned grid = (unsigned)((rows + R - 1) / R);
-  hipLaunchKernelGGL(merge_kernel<KP>, dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, rows, out, lse_out);
+  hipLaunchKernelGGL(merge_kernel<KP>, dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, B, Hq, h0, hn, out,
+                     lse_out);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t rows, float* out, float* lse_out,
-                        hipStream_t stream) {
+hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn,
+                        float* out, float* lse_out, hipStream_t stream) {
+  const int64_t rows = B * hn;
   if (rows == 0) return hipSuccess;
   // With enough rows to fill the GPU, one thread group per row streams best.
   // With few rows (long ranges of few sequences), spread a row's parts over
   // up to 8 thread groups, at least 2 parts each.
   if (rows < 4096) {
-    if (n_parts >= 16) return launch<8>(outs, lses, n_parts, rows, out, lse_out, stream);
-    if (n_parts >= 8) return launch<4>(outs, lses, n_parts, rows, out, lse_out, stream);
-    if (n_parts >= 4) return launch<2>(outs, lses, n_parts, rows, out, lse_out, stream);
+    if (n_parts >= 16) return launch<8>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
+    if (n_parts >= 8) return launch<4>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
+    if (n_parts >= 4) return launch<2>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
   }
-  return launch<1>(outs, lses, n_parts, rows, out, lse_out, stream);
+  return launch<1>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
 }
 
 }  // namespace bana

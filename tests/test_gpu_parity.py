@@ -349,3 +349,24 @@ def test_migration_bit_exact_and_attention_unchanged(name, part):
     op, lp, _, _ = dw.results()
     assert np.array_equal(o1.cpu().numpy(), op[part], equal_nan=True)
     assert np.array_equal(l1.cpu().numpy(), lp[part], equal_nan=True)
+
+
+@pytest.mark.parametrize("name,part,split", [("tiny", 0, 1), ("llama3_8b", 0, 3), ("long", 0, 5), ("mixed", 1, 4)])
+def test_head_split_concatenates_to_unsplit_bit_exact(name, part, split):
+    """Head partitions (the literal head-dimension split): complementary kv-head ranges give the
+    full partition result bit for bit, and a call leaves the rows of other heads untouched."""
+    w = _workload(name)
+    dw = DeviceWorkload(w)
+    op, lp, _, _ = dw.results()
+    B, Hq, G = w.batch, w.num_q_heads, w.group
+    out = torch.full((B, Hq, 128), float("nan"), dtype=torch.float32, device="cuda")
+    lse = torch.full((B, Hq), float("nan"), dtype=torch.float32, device="cuda")
+    args = (dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin[part], dw.kv_end[part])
+    _log(f"[heads] {name} part {part} split at kv head {split}")
+    bana.bana_decode_attn_heads(*args, 0, split, out, lse, workspace=dw.workspace, dims=dw.dims[part])
+    o = out.cpu().numpy()
+    assert np.all(np.isnan(o[:, split * G:])) and np.all(np.isnan(lse.cpu().numpy()[:, split * G:]))
+    assert np.array_equal(o[:, :split * G], op[part][:, :split * G])
+    bana.bana_decode_attn_heads(*args, split, w.num_kv_heads, out, lse, workspace=dw.workspace, dims=dw.dims[part])
+    assert np.array_equal(out.cpu().numpy(), op[part])
+    assert np.array_equal(lse.cpu().numpy(), lp[part])

@@ -140,6 +140,20 @@ def test_migrate_rejects_bad_arguments(lib):
     assert lib.bana_migrate_kv_blocks(ctypes.byref(_dims(batch=70000)), *args, 10, FAKE, FAKE, None) == -2
 
 
+def test_heads_rejects_bad_ranges(lib):
+    d = _dims()  # 2 kv heads
+
+    def heads(h0, h1, dd=d):
+        return lib.bana_decode_attn_heads(ctypes.byref(dd), *[FAKE] * 7, h0, h1, FAKE, FAKE, None, 0, None)
+
+    assert heads(-1, 1) == -1
+    assert heads(0, 3) == -1
+    assert heads(2, 1) == -1
+    assert heads(1, 1) == 0  # empty head range: nothing to do, no launch
+    assert heads(0, 2, _dims(head_dim=64)) == -2
+    assert lib.bana_decode_attn_heads(ctypes.byref(d), *[FAKE] * 7, 0, 2, None, FAKE, None, 0, None) == -1
+
+
 def test_negative_total_hint_rejected(lib):
     d = _dims()
     d.total_range_tokens = -1
