@@ -38,7 +38,7 @@ def _parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="llama3_8b", choices=["tiny", "llama3_8b", "long", "mixed", "fine"])
+    ap.add_argument("--config", default="llama3_8b", choices=["tiny", "llama3_8b", "long", "mixed", "fine", "mha13b"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU time of the oracle baseline")

@@ -146,6 +146,9 @@ CONFIGS: Dict[str, Config] = {
     "long": Config(3, "long", 8, 32, 8, 131072),
     "mixed": Config(4, "mixed", 256, 32, 8, 16384),
     "fine": Config(5, "fine", 512, 64, 8, 2048, key_bias_std=2.0),
+    # Multi-head (G = 1) layer with the public LLaMA-13B / OPT-13B head layout (40 heads x 128), the
+    # models the paper evaluates; 2048-token contexts, last 30 % of the blocks migrated.
+    "mha13b": Config(6, "mha13b", 32, 40, 40, 2048),
 }
 
 
@@ -169,11 +172,12 @@ def _lens_and_ranges(cfg: Config, seed: int) -> Tuple[np.ndarray, np.ndarray, np
             nb = _nblk(int(L))
             j = int(rs.integers(1, nb - 1, endpoint=True))
             parts.append(_split_at_block(int(L), j))
-    elif cfg.name == "llama3_8b":
-        lens = np.full(B, 4096)
-        nb = 256
+    elif cfg.name in ("llama3_8b", "mha13b"):
+        L = cfg.max_seq_len
+        lens = np.full(B, L)
+        nb = L // BLOCK_SIZE
         migrated = int(round(0.3 * nb))
-        parts = [_split_at_block(4096, nb - migrated) for _ in range(B)]
+        parts = [_split_at_block(L, nb - migrated) for _ in range(B)]
     elif cfg.name == "long":
         lens = rl.integers(32768, 131072, size=B, endpoint=True)
         parts = []

@@ -101,7 +101,7 @@ def test_tiny_parity(seed):
     _full_parity(_workload("tiny", seed))
 
 
-@pytest.mark.parametrize("name", ["llama3_8b", "long", "mixed", "fine"])
+@pytest.mark.parametrize("name", ["llama3_8b", "long", "mixed", "fine", "mha13b"])
 def test_config_parity(name):
     _full_parity(_workload(name))
 
