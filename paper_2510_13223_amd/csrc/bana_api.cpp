@@ -57,12 +57,19 @@ struct Plan {
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 // Workgroups are (chunk, sequence, kv head) with `waves` wavefronts each.
-// Aim for one full round of resident wavefronts: enough waves per
-// (sequence, kv head) pair to cover the GPU, and a per-wavefront share of
-// the call's blocks (from the total-tokens hint) that every range is cut
-// to, so a long range is spread over several workgroups instead of keeping
-// a few wavefronts busy after the rest have finished.  Short ranges keep
-// a single chunk.  Without hints the table width bounds the range length.
+// Aim for one full round of resident wavefronts (256 CUs x 16).  With the
+// range hints (longest range, total tokens):
+//  - uneven ranges (longest > 1.25 x mean) get 8 waves per workgroup, so the
+//    long ranges finish early while short ones fill the rest of the GPU;
+//  - when the (sequence, kv head) pairs alone cannot fill the round, every
+//    range is cut into chunks of one wavefront's even share of the call's
+//    blocks, enlarged so the rounding of each range to whole chunks still
+//    fits one round (a second, partly filled round would double the time of
+//    its workgroups);
+//  - otherwise a range is only cut when its workgroup would take more than
+//    twice the even share, into chunks of twice the even share.
+// Chunks need workspace; without it the call runs unsplit.  Without hints
+// the table width bounds the range length.
 Plan make_plan(const bana_dims* d) {
   const int64_t pairs = (int64_t)d->batch * d->num_kv_heads;
   int64_t bound = d->max_blocks_per_seq;  // blocks of the longest range
@@ -70,9 +77,15 @@ Plan make_plan(const bana_dims* d) {
   bound = std::max<int64_t>(bound, 1);
   int64_t wpp = (kTargetWaves + pairs - 1) / pairs;
   wpp = std::max<int64_t>(1, std::min<int64_t>(wpp, std::max<int64_t>(1, bound / kMinBlocksPerWave)));
+  const bool hinted = d->total_range_tokens > 0;
+  const int64_t mean_blocks =
+      hinted ? std::max<int64_t>(1, d->total_range_tokens / (kBlockSize * (int64_t)d->batch) + 1) : bound;
+  const bool uneven = hinted && 4 * bound > 5 * mean_blocks;
   Plan p;
   if (d->waves_hint > 0)
     p.waves = d->waves_hint;
+  else if (uneven && bound >= 8 * kMinBlocksPerWave)
+    p.waves = 8;
   else
     p.waves = wpp >= 8 ? 8 : wpp >= 4 ? 4 : wpp >= 2 ? 2 : 1;
   // The cross-wave combine keeps W * G rows of 132 floats in LDS; stay within 64 KiB per workgroup.
@@ -81,18 +94,20 @@ Plan make_plan(const bana_dims* d) {
   if (d->chunks_hint > 0) {
     p.nc = d->chunks_hint;
     p.cmin = 1;
-  } else if (d->total_range_tokens > 0) {
+  } else if (hinted) {
     // (block, kv head) units of the call and the blocks per wavefront if they
     // were spread evenly over one round of resident wavefronts.
-    const int64_t mean_blocks = std::max<int64_t>(1, d->total_range_tokens / (kBlockSize * (int64_t)d->batch) + 1);
     const int64_t units = mean_blocks * pairs;
-    int64_t per_wave = (units + kTargetWaves - 1) / kTargetWaves;
-    // Rounding each range up to whole chunks adds at most one workgroup per
-    // (sequence, kv head) pair: leave that many slots free so the call still
-    // fits one dispatch round (a second, partly filled round would double
-    // the time of its workgroups).
+    const int64_t even = (units + kTargetWaves - 1) / kTargetWaves;
     const int64_t slots = kTargetWaves / p.waves;
-    if (pairs < slots) per_wave = std::max<int64_t>(per_wave, (units + p.waves * (slots - pairs) - 1) / (p.waves * (slots - pairs)));
+    int64_t per_wave;
+    if (pairs < slots) {
+      per_wave = std::max<int64_t>(even, (units + p.waves * (slots - pairs) - 1) / (p.waves * (slots - pairs)));
+    } else if (bound > 2 * even * p.waves) {
+      per_wave = 2 * even;
+    } else {
+      per_wave = bound;  // one chunk per range
+    }
     per_wave = std::max<int64_t>(kMinBlocksPerWave, per_wave);
     const int64_t chunk = per_wave * p.waves;
     p.nc = ceil_div(bound, chunk);
