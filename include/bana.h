@@ -202,6 +202,19 @@ bana_status bana_migrate_kv_blocks(const bana_dims* d, const void* src_k_cache, 
                                    const int32_t* dst_block_table, int64_t dst_num_blocks,
                                    const int32_t* blk_begin, const int32_t* blk_end, void* stream);
 
+/*
+ * Stream-ordered copy of `bytes` bytes from src to dst by a small kernel
+ * (at most 64 workgroups), for staging KV between a host-side store and the
+ * device pools in the layer-wise pipeline of Sec. 4.2 (fetch of layer i+1
+ * and store of layer i-1 beside the attention of layer i).  Either side may
+ * be device memory or pinned host memory (hipHostMalloc, reached over the
+ * host link).  Being a kernel, the copy is ordered on `stream` like the
+ * attention calls and waits for other streams only through device-side
+ * events.  bytes must be a multiple of 16 and both pointers 16-byte aligned
+ * (else BANA_ERR_INVALID); the ranges must not overlap.
+ */
+bana_status bana_copy_async(void* dst, const void* src, size_t bytes, void* stream);
+
 /* Static text for a status code. */
 const char* bana_status_string(bana_status s);
 

@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
     L.bana_decode_attn_heads.restype = ctypes.c_int
     L.bana_migrate_kv_blocks.argtypes = [D, P, P, P, P, P, P, ctypes.c_int64, P, P, P]
     L.bana_migrate_kv_blocks.restype = ctypes.c_int
+    L.bana_copy_async.argtypes = [P, P, ctypes.c_size_t, P]
+    L.bana_copy_async.restype = ctypes.c_int
     L.bana_debug_kv_rows.argtypes = [D, P, P, P, P, P]
     L.bana_debug_kv_rows.restype = ctypes.c_int
     _lib = L

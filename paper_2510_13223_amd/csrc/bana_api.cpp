@@ -294,6 +294,11 @@ bana_status bana_migrate_kv_blocks(const bana_dims* d, const void* src_k_cache, 
                                             (int)maxb, d->num_kv_heads, static_cast<hipStream_t>(stream)));
 }
 
+bana_status bana_copy_async(void* dst, const void* src, size_t bytes, void* stream) {
+  if (!dst || !src || bytes % 16 != 0 || !aligned16(dst) || !aligned16(src)) return BANA_ERR_INVALID;
+  return device_status(bana::launch_copy(dst, src, bytes, static_cast<hipStream_t>(stream)));
+}
+
 bana_status bana_debug_kv_rows(const bana_dims* d, const int32_t* block_table, const int32_t* kv_range_begin,
                                const int32_t* kv_range_end, int64_t* rows_out, void* stream) {
   const bana_status st = check_dims(d);

@@ -37,6 +37,10 @@ hipError_t launch_migrate(const void* src_k, const void* src_v, const int32_t* s
                           const int32_t* dst_table, const int32_t* blk_begin, const int32_t* blk_end, int B,
                           int max_blocks, int max_migrated_blocks, int Hkv, hipStream_t stream);
 
+// Stream-ordered copy of `bytes` (a multiple of 16) between 16-byte aligned buffers in device or
+// pinned host memory, by a small kernel.
+hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
+
 // Address export for the tests (rows of the K pool visited per logical token).
 hipError_t launch_debug_rows(const int32_t* table, const int32_t* begin, const int32_t* end, int B, int Hkv,
                              int max_blocks, int64_t* rows, hipStream_t stream);

@@ -14,6 +14,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "kernels.h"
 #include "paged_addr.h"
 
@@ -66,7 +68,35 @@ __global__ __launch_bounds__(kThreads) void migrate_kernel(const u32x4* __restri
   }
 }
 
+// Stream-ordered copy of n16 16-byte units by a grid-stride loop; either side may be device memory
+// or pinned host memory (reached over the host link).
+__global__ __launch_bounds__(kThreads) void copy_kernel(u32x4* __restrict__ dst, const u32x4* __restrict__ src,
+                                                        int64_t n16) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t i0 = (int64_t)blockIdx.x * kThreads + threadIdx.x; i0 < n16; i0 += stride * kUnroll) {
+    u32x4 x[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+      if (i0 + u * stride < n16) x[u] = __builtin_nontemporal_load(src + i0 + u * stride);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+      if (i0 + u * stride < n16) __builtin_nontemporal_store(x[u], dst + i0 + u * stride);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+  const int64_t n16 = (int64_t)(bytes / 16);
+  if (n16 == 0) return hipSuccess;
+  // A few workgroups only: enough to fill the host link, few enough to leave the CUs to the
+  // attention kernel that runs beside the copy.
+  const int64_t per_wg = (int64_t)kThreads * kUnroll;
+  const unsigned grid = (unsigned)std::min<int64_t>(64, (n16 + per_wg - 1) / per_wg);
+  hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(kThreads), 0, stream, static_cast<u32x4*>(dst),
+                     static_cast<const u32x4*>(src), n16);
+  return hipGetLastError();
+}
 
 hipError_t launch_migrate(const void* src_k, const void* src_v, const int32_t* src_table, void* dst_k, void* dst_v,
                           const int32_t* dst_table, const int32_t* blk_begin, const int32_t* blk_end, int B,

@@ -415,3 +415,57 @@ def make_migration(w: Workload, part: int, seed: int = 0, pool_factor: float = 1
     dk = np.full((nb,) + w.k_cache.shape[1:], SENTINEL, dtype=np.uint16)
     dv = np.full((nb,) + w.v_cache.shape[1:], SENTINEL, dtype=np.uint16)
     return Migration(dk, dv, table, begin, end)
+
+
+@dataclasses.dataclass
+class LayerStore:
+    """Host-side KV store for a layer-wise pipeline over a workload.
+
+    The first `fetch_blocks` logical blocks of sequence 0 are prefix-cache hits
+    held in the store (fetched host-to-device before each layer's attention);
+    the `store_blocks` blocks after them are newly computed and stored back
+    device-to-host after the layer.  The workload is re-placed so both groups
+    are contiguous physical runs (fetch: blocks [0, fetch_blocks), store: the
+    next `store_blocks`), one copy each per pool.  Every layer has its own
+    fetched contents.
+    """
+    w: Workload
+    num_layers: int
+    fetch_blocks: int
+    store_blocks: int
+    fetch_k: np.ndarray  # [layers, fetch_blocks, Hkv, D/8, bs, 8]
+    fetch_v: np.ndarray  # [layers, fetch_blocks, Hkv, D, bs]
+
+
+def make_layer_store(w: Workload, num_layers: int, fetch_tokens: int, store_tokens: int, seed: int = 0) -> LayerStore:
+    fb = (fetch_tokens + BLOCK_SIZE - 1) // BLOCK_SIZE
+    sb = (store_tokens + BLOCK_SIZE - 1) // BLOCK_SIZE
+    if fb + sb > int(np.sum(w.block_table[0] >= 0)):
+        raise ValueError("sequence 0 is shorter than the fetched + stored blocks")
+    # Physical permutation moving sequence 0's blocks 0 .. fb + sb - 1 to physical blocks 0 .. fb + sb - 1.
+    want = w.block_table[0, :fb + sb].astype(np.int64)
+    others = np.setdiff1d(np.arange(w.num_blocks), want, assume_unique=False)
+    order = np.concatenate([want, others])  # new physical i holds old physical order[i]
+    perm = np.empty(w.num_blocks, dtype=np.int64)
+    perm[order] = np.arange(w.num_blocks)
+    k2 = w.k_cache[order]
+    v2 = w.v_cache[order]
+    t2 = np.where(w.block_table >= 0, perm[np.maximum(w.block_table, 0)], -1).astype(np.int32)
+    w2 = dataclasses.replace(w, k_cache=k2, v_cache=v2, block_table=t2)
+    Hkv = w.num_kv_heads
+    fk = np.empty((num_layers, fb) + w.k_cache.shape[1:], dtype=np.uint16)
+    fv = np.empty((num_layers, fb) + w.v_cache.shape[1:], dtype=np.uint16)
+    for layer in range(num_layers):
+        kk = _gen_normal_bf16(seed, 3000 + layer, _S_K, -1, (fb, Hkv, BLOCK_SIZE, HEAD_DIM))
+        fk[layer] = kk.reshape(fb, Hkv, BLOCK_SIZE, HEAD_DIM // K_CHUNK, K_CHUNK).transpose(0, 1, 3, 2, 4)
+        fv[layer] = _gen_normal_bf16(seed, 3000 + layer, _S_V, -1, (fb, Hkv, BLOCK_SIZE, HEAD_DIM)).transpose(0, 1, 3, 2)
+    return LayerStore(w2, num_layers, fb, sb, fk, fv)
+
+
+def layer_view(store: LayerStore, layer: int) -> Workload:
+    """The workload as layer `layer` sees it: its fetched prefix blocks in place."""
+    k = store.w.k_cache.copy()
+    v = store.w.v_cache.copy()
+    k[:store.fetch_blocks] = store.fetch_k[layer]
+    v[:store.fetch_blocks] = store.fetch_v[layer]
+    return dataclasses.replace(store.w, k_cache=k, v_cache=v)

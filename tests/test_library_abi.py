@@ -154,6 +154,13 @@ def test_heads_rejects_bad_ranges(lib):
     assert lib.bana_decode_attn_heads(ctypes.byref(d), *[FAKE] * 7, 0, 2, None, FAKE, None, 0, None) == -1
 
 
+def test_copy_rejects_bad_arguments(lib):
+    assert lib.bana_copy_async(None, FAKE, 64, None) == -1
+    assert lib.bana_copy_async(FAKE, None, 64, None) == -1
+    assert lib.bana_copy_async(FAKE, FAKE, 24, None) == -1
+    assert lib.bana_copy_async(ctypes.c_void_p(0x100008), FAKE, 64, None) == -1
+
+
 def test_negative_total_hint_rejected(lib):
     d = _dims()
     d.total_range_tokens = -1
