@@ -27,10 +27,11 @@
  *    group (num_q_heads / num_kv_heads) above 16.
  *  - A failed launch returns BANA_ERR_DEVICE; bana_last_error() then holds
  *    the HIP error text (per calling thread).
- *  - Device-resident values are preconditions and are not checked:
+ *  - Device-resident values are preconditions and are not checked per call:
  *    0 <= kv_range_begin[b] <= kv_range_end[b] <= seq_lens[b], and every
  *    block-table entry for a block that overlaps [begin, end) names a block
  *    of the pool.  Entries outside the covered blocks are never read.
+ *    bana_validate_ranges checks them on the device when wanted.
  *
  * Layouts (bf16 = IEEE binary16-brain, stored as 2 bytes)
  * --------------------------------------------------------
@@ -201,6 +202,23 @@ bana_status bana_migrate_kv_blocks(const bana_dims* d, const void* src_k_cache, 
                                    const int32_t* src_block_table, void* dst_k_cache, void* dst_v_cache,
                                    const int32_t* dst_block_table, int64_t dst_num_blocks,
                                    const int32_t* blk_begin, const int32_t* blk_end, void* stream);
+
+/*
+ * Device-side check of the preconditions the attention and migration calls
+ * trust (they are not checked per call, to keep calls free of host
+ * synchronisation).  Writes to *result (int32 in device memory) 0 when, for
+ * every partition p < n_parts and sequence b,
+ *   0 <= seq_lens[b] <= max_blocks_per_seq * block_size            (else 3)
+ *   0 <= kv_range_begin[p][b] <= kv_range_end[p][b]                (else 1)
+ *   kv_range_end[p][b] <= seq_lens[b]                               (else 2)
+ *   every block overlapping the range maps into [0, num_blocks)     (else 4)
+ * and otherwise the highest code found.  Asynchronous on `stream`; read
+ * *result after synchronising.  Table entries outside checked ranges are
+ * never read.  More than 65535 partitions gives BANA_ERR_UNSUPPORTED.
+ */
+bana_status bana_validate_ranges(const bana_dims* d, const int32_t* block_table, const int32_t* seq_lens,
+                                 const int32_t* kv_range_begin, const int32_t* kv_range_end, int32_t n_parts,
+                                 int32_t* result, void* stream);
 
 /*
  * Stream-ordered copy of `bytes` bytes from src to dst by a small kernel

@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
     L.bana_decode_attn_heads.restype = ctypes.c_int
     L.bana_migrate_kv_blocks.argtypes = [D, P, P, P, P, P, P, ctypes.c_int64, P, P, P]
     L.bana_migrate_kv_blocks.restype = ctypes.c_int
+    L.bana_validate_ranges.argtypes = [D, P, P, P, P, ctypes.c_int32, P, P]
+    L.bana_validate_ranges.restype = ctypes.c_int
     L.bana_copy_async.argtypes = [P, P, ctypes.c_size_t, P]
     L.bana_copy_async.restype = ctypes.c_int
     L.bana_debug_kv_rows.argtypes = [D, P, P, P, P, P]
@@ -269,6 +271,25 @@ def bana_migrate_kv_blocks(src_k, src_v, src_table, dst_k, dst_v, dst_table, blk
                                       _stream(stream))
     if st != BANA_OK:
         raise BanaError(st, "bana_migrate_kv_blocks")
+
+
+def bana_validate_ranges(block_table, seq_lens, kv_range_begin, kv_range_end, num_blocks: int, result,
+                         stream=None) -> None:
+    """Device-side precondition check; ``result`` (int32 [1]) receives 0 or a rule code (include/bana.h)."""
+    B, mb = block_table.shape
+    if kv_range_begin.dim() == 1:
+        kv_range_begin, kv_range_end = kv_range_begin[None], kv_range_end[None]
+    n = kv_range_begin.shape[0]
+    _need(block_table, "block_table", torch.int32)
+    _need(seq_lens, "seq_lens", torch.int32, (B,))
+    _need(kv_range_begin, "kv_range_begin", torch.int32, (n, B))
+    _need(kv_range_end, "kv_range_end", torch.int32, (n, B))
+    _need(result, "result", torch.int32, (1,))
+    dims = bana_dims(B, 1, 1, HEAD_DIM, BLOCK_SIZE, mb, num_blocks, 0, 0, 0, 0, 0)
+    st = lib().bana_validate_ranges(ctypes.byref(dims), _ptr(block_table), _ptr(seq_lens), _ptr(kv_range_begin),
+                                    _ptr(kv_range_end), n, _ptr(result), _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_validate_ranges")
 
 
 def bana_debug_kv_rows(block_table, kv_range_begin, kv_range_end, num_blocks: int, num_kv_heads: int, rows_out,

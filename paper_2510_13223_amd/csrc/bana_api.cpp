@@ -294,6 +294,18 @@ bana_status bana_migrate_kv_blocks(const bana_dims* d, const void* src_k_cache, 
                                             (int)maxb, d->num_kv_heads, static_cast<hipStream_t>(stream)));
 }
 
+bana_status bana_validate_ranges(const bana_dims* d, const int32_t* block_table, const int32_t* seq_lens,
+                                 const int32_t* kv_range_begin, const int32_t* kv_range_end, int32_t n_parts,
+                                 int32_t* result, void* stream) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!block_table || !seq_lens || !kv_range_begin || !kv_range_end || !result || n_parts < 1) return BANA_ERR_INVALID;
+  if (n_parts > 65535) return BANA_ERR_UNSUPPORTED;  // one grid row per partition
+  return device_status(bana::launch_validate(block_table, seq_lens, kv_range_begin, kv_range_end, n_parts, d->batch,
+                                             d->max_blocks_per_seq, d->num_blocks, result,
+                                             static_cast<hipStream_t>(stream)));
+}
+
 bana_status bana_copy_async(void* dst, const void* src, size_t bytes, void* stream) {
   if (!dst || !src || bytes % 16 != 0 || !aligned16(dst) || !aligned16(src)) return BANA_ERR_INVALID;
   return device_status(bana::launch_copy(dst, src, bytes, static_cast<hipStream_t>(stream)));

@@ -41,6 +41,12 @@ hipError_t launch_migrate(const void* src_k, const void* src_v, const int32_t* s
 // pinned host memory, by a small kernel.
 hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
 
+// Device-side check of ranges, lengths and table entries; writes 0 or the highest broken-rule code
+// to *result (device memory).
+hipError_t launch_validate(const int32_t* table, const int32_t* seq_lens, const int32_t* begin, const int32_t* end,
+                           int n_parts, int B, int max_blocks, int64_t num_blocks, int32_t* result,
+                           hipStream_t stream);
+
 // Address export for the tests (rows of the K pool visited per logical token).
 hipError_t launch_debug_rows(const int32_t* table, const int32_t* begin, const int32_t* end, int B, int Hkv,
                              int max_blocks, int64_t* rows, hipStream_t stream);

@@ -431,3 +431,85 @@ def test_layer_pipeline_matches_serial_and_oracle():
     assert pipe.stage_ms.shape == (st.num_layers, 3)
     # layers see different fetched prefixes, so their outputs differ
     assert not np.array_equal(po[0], po[1])
+
+
+def test_pool_beyond_4gib_uses_64bit_offsets():
+    """Blocks placed beyond 2^31 bf16 elements of a pool (a 4.6 GB pool per cache) attend, migrate
+    and export addresses exactly as the same blocks in a compact pool."""
+    lens = [500, 333, 1000, 17]
+    ranges = [[(0, 256), (0, 100), (0, 500), (0, 17)], [(256, 500), (100, 333), (500, 1000), (17, 17)]]
+    w = W.make_custom(7, 4, 32, 8, lens, ranges, q_scale=1 / math.sqrt(128))
+    base = 135000  # 135000 blocks x 8 kv heads x 2048 elements > 2^31
+    big_nb = base + w.num_blocks
+    _log(f"[64-bit] pools of {big_nb} blocks ({big_nb * 8 * 4096 / 1e9:.1f} GB each)")
+    small = DeviceWorkload(w)
+    ref = small.results()
+    big_k = torch.full((big_nb,) + tuple(small.k_cache.shape[1:]), float("nan"), dtype=torch.bfloat16, device="cuda")
+    big_v = torch.full((big_nb,) + tuple(small.v_cache.shape[1:]), float("nan"), dtype=torch.bfloat16, device="cuda")
+    big_k[base:] = small.k_cache
+    big_v[base:] = small.v_cache
+    table = torch.where(small.block_table >= 0, small.block_table + base, small.block_table).contiguous()
+    B, Hq = w.batch, w.num_q_heads
+    for p in range(w.n_parts):
+        o = torch.empty((B, Hq, 128), dtype=torch.float32, device="cuda")
+        l = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+        d = bana.make_dims(B, Hq, 8, w.max_blocks_per_seq, big_nb, max_range_tokens=small.dims[p].max_range_tokens,
+                           total_range_tokens=small.dims[p].total_range_tokens)
+        bana.bana_decode_attn_partial(small.q, big_k, big_v, table, small.seq_lens, small.kv_begin[p],
+                                      small.kv_end[p], o, l, workspace=small.workspace, dims=d)
+        assert np.array_equal(o.cpu().numpy(), ref[0][p]) and np.array_equal(l.cpu().numpy(), ref[1][p])
+        rows = torch.empty((B, 8, w.max_blocks_per_seq * 16), dtype=torch.int64, device="cuda")
+        bana.bana_debug_kv_rows(table, small.kv_begin[p], small.kv_end[p], big_nb, 8, rows)
+        expect = oracle.kv_rows(table.cpu().numpy(), big_nb, 8, w.kv_begin[p], w.kv_end[p])
+        assert expect.max() > 2 ** 31 // 128
+        np.testing.assert_array_equal(rows.cpu().numpy(), expect)
+    # migrate the blocks of partition 1 from the far end of the big pools into a compact pool
+    m = W.make_migration(w, 1, seed=2)
+    dk = torch.from_numpy(m.dst_k.view(np.int16)).view(torch.bfloat16).cuda()
+    dv = torch.from_numpy(m.dst_v.view(np.int16)).view(torch.bfloat16).cuda()
+    bana.bana_migrate_kv_blocks(big_k, big_v, table, dk, dv, torch.from_numpy(m.dst_table).cuda(),
+                                torch.from_numpy(m.blk_begin).cuda(), torch.from_numpy(m.blk_end).cuda())
+    ek, ev = oracle.migrate(w.k_cache, w.v_cache, w.block_table, m.dst_k, m.dst_v, m.dst_table, m.blk_begin,
+                            m.blk_end)
+    np.testing.assert_array_equal(dk.cpu().view(torch.int16).numpy().view(np.uint16), ek)
+    np.testing.assert_array_equal(dv.cpu().view(torch.int16).numpy().view(np.uint16), ev)
+    del big_k, big_v
+    torch.cuda.empty_cache()
+
+
+def test_validate_ranges_codes():
+    w = _workload("tiny", 0)
+    dw = DeviceWorkload(w)
+    res = torch.empty(1, dtype=torch.int32, device="cuda")
+
+    def check(table, lens, begin, end, nb=w.num_blocks):
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+        bana.bana_validate_ranges(t(table), t(lens), t(begin), t(end), nb, res)
+        torch.cuda.synchronize()
+        return int(res.item())
+
+    tb, L, b0, e0 = w.block_table, w.seq_lens, w.kv_begin, w.kv_end
+    assert check(tb, L, b0, e0) == 0
+    assert check(tb, L, b0[0], e0[0]) == 0
+    bad = b0.copy(); bad[1, 2] = e0[1, 2] + 1
+    assert check(tb, L, bad, e0) == 1
+    bad = b0.copy(); bad[0, 0] = -3
+    assert check(tb, L, bad, e0) == 1
+    bad = e0.copy(); bad[1, 3] = L[3] + 5
+    assert check(tb, L, b0, bad) == 2
+    lens = L.copy(); lens[0] = w.max_blocks_per_seq * 16 + 1
+    assert check(tb, lens, b0, e0) == 3
+    tbl = tb.copy(); tbl[2, 3] = -1
+    assert check(tbl, L, b0, e0) == 4
+    tbl = tb.copy(); tbl[1, 0] = w.num_blocks
+    assert check(tbl, L, b0, e0) == 4
+    bad = b0.copy(); bad[0, 0] = e0[0, 0] + 1  # sequence 0 breaks rule 1, sequence 1's table rule 4
+    assert check(tbl, L, bad, e0) == 4  # the highest code wins
+    # entries past a range are never read: poison them, still valid
+    tbl = tb.copy()
+    for b in range(w.batch):
+        tbl[b, (L[b] + 15) // 16:] = 1 << 30
+    assert check(tbl, L, b0, e0) == 0
+    for name in ("llama3_8b", "mixed"):
+        ww = _workload(name)
+        assert check(ww.block_table, ww.seq_lens, ww.kv_begin, ww.kv_end, ww.num_blocks) == 0

@@ -154,6 +154,16 @@ def test_heads_rejects_bad_ranges(lib):
     assert lib.bana_decode_attn_heads(ctypes.byref(d), *[FAKE] * 7, 0, 2, None, FAKE, None, 0, None) == -1
 
 
+def test_validate_rejects_bad_arguments(lib):
+    d = _dims()
+    assert lib.bana_validate_ranges(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 0, FAKE, None) == -1
+    for i in range(5):
+        a = [FAKE] * 5
+        a[i] = None
+        assert lib.bana_validate_ranges(ctypes.byref(d), *a[:4], 1, a[4], None) == -1, i
+    assert lib.bana_validate_ranges(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 70000, FAKE, None) == -2
+
+
 def test_copy_rejects_bad_arguments(lib):
     assert lib.bana_copy_async(None, FAKE, 64, None) == -1
     assert lib.bana_copy_async(FAKE, None, 64, None) == -1
