@@ -87,6 +87,11 @@ typedef struct {
   int32_t chunks_hint;        /* chunks a range may be split into (needs workspace) */
   int32_t reserved;           /* must be 0 */
   int64_t total_range_tokens; /* sum over sequences of kv_range_end - kv_range_begin */
+  /* Optional device array [batch]: the order in which sequences are
+   * dispatched (a permutation of 0..batch-1; longest range first lets the
+   * short ones fill the end of the launch).  NULL = natural order.  Results
+   * do not depend on it. */
+  const int32_t* seq_order;
 } bana_dims;
 
 /*

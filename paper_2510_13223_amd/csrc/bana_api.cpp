@@ -179,6 +179,7 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
   a.begin = kv_range_begin;
   a.end = kv_range_end;
   a.n_parts = n_parts;
+  a.seq_order = d->seq_order;
   a.B = d->batch;
   a.Hq = d->num_q_heads;
   a.Hkv = d->num_kv_heads;

@@ -15,6 +15,7 @@ struct PartialArgs {
   const int32_t* begin;     // [n_parts][B]
   const int32_t* end;       // [n_parts][B]
   int n_parts;              // ranges per sequence, 1..64
+  const int32_t* seq_order; // optional [B] dispatch order of sequences (NULL: natural)
   float* out;               // nc == 1: final output [B][Hq][128]; nc > 1: chunk partials [nc][B][Hq][128]
   float* lse;               // nc == 1: final lse [B][Hq];               nc > 1: chunk lses [nc][B][Hq]
   int B, Hq, Hkv, G, max_blocks;

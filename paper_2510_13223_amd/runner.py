@@ -30,7 +30,7 @@ class DeviceWorkload:
     """Device-resident inputs and outputs of one workload, plus prepared call arguments."""
 
     def __init__(self, w, device="cuda", waves_hint: int = 0, chunks_hint: int = 0, use_workspace: bool = True,
-                 range_hints: bool = True):
+                 range_hints: bool = True, order_hints: bool = True):
         self.w = w
         self.device = torch.device(device)
         self.q = _bf16(w.q, self.device)
@@ -46,19 +46,31 @@ class DeviceWorkload:
         self.out = torch.empty((B, Hq, bana.HEAD_DIM), dtype=torch.float32, device=self.device)
         self.lse_out = torch.empty((B, Hq), dtype=torch.float32, device=self.device)
 
+        # Dispatch order hints: sequences with the longest range first (stable), so short ones fill
+        # the end of each launch.  Results do not depend on the order.
+        def order(lens):
+            if not order_hints:
+                return None
+            return torch.from_numpy(np.argsort(-lens, kind="stable").astype(np.int32)).to(self.device)
+
         self.dims: List[bana.bana_dims] = []
+        self._orders = []
         for p in range(P):
             lens = w.kv_end[p].astype(np.int64) - w.kv_begin[p]
+            self._orders.append(order(lens))
             self.dims.append(bana.make_dims(B, Hq, w.num_kv_heads, w.max_blocks_per_seq, w.num_blocks,
                                             max_range_tokens=int(lens.max()) if range_hints else 0,
                                             waves_hint=waves_hint, chunks_hint=chunks_hint,
-                                            total_range_tokens=int(lens.sum()) if range_hints else 0))
+                                            total_range_tokens=int(lens.sum()) if range_hints else 0,
+                                            seq_order=self._orders[-1]))
         # The fused call sees each sequence's ranges as one concatenated range.
         lens_all = (w.kv_end.astype(np.int64) - w.kv_begin).sum(axis=0)
+        self._orders.append(order(lens_all))
         self.fused_dims = bana.make_dims(B, Hq, w.num_kv_heads, w.max_blocks_per_seq, w.num_blocks,
                                          max_range_tokens=int(lens_all.max()) if range_hints else 0,
                                          waves_hint=waves_hint, chunks_hint=chunks_hint,
-                                         total_range_tokens=int(lens_all.sum()) if range_hints else 0)
+                                         total_range_tokens=int(lens_all.sum()) if range_hints else 0,
+                                         seq_order=self._orders[-1])
         self.fused_out = torch.empty((B, Hq, bana.HEAD_DIM), dtype=torch.float32, device=self.device)
         self.fused_lse = torch.empty((B, Hq), dtype=torch.float32, device=self.device)
         ws = max(bana.bana_decode_attn_workspace_bytes(d) for d in self.dims + [self.fused_dims]) if use_workspace else 0
@@ -89,7 +101,7 @@ class DeviceWorkload:
                 vp(self.seq_lens), vp(self.kv_begin[p]), vp(self.kv_end[p]), vp(self.out_partials[p]),
                 vp(self.lses[p]), ws_ptr, ws_bytes])
         B, Hq = self.w.batch, self.w.num_q_heads
-        self._merge_dims = bana.bana_dims(B, Hq, 1, bana.HEAD_DIM, bana.BLOCK_SIZE, 1, 1, 0, 0, 0, 0, 0)
+        self._merge_dims = bana.bana_dims(B, Hq, 1, bana.HEAD_DIM, bana.BLOCK_SIZE, 1, 1, 0, 0, 0, 0, 0, None)
         self._merge_args = [ctypes.byref(self._merge_dims), vp(self.out_partials), vp(self.lses), self.w.n_parts,
                             vp(self.out), vp(self.lse_out)]
         self._fused_args = [ctypes.byref(self.fused_dims), vp(self.q), vp(self.k_cache), vp(self.v_cache),

@@ -513,3 +513,15 @@ def test_validate_ranges_codes():
     for name in ("llama3_8b", "mixed"):
         ww = _workload(name)
         assert check(ww.block_table, ww.seq_lens, ww.kv_begin, ww.kv_end, ww.num_blocks) == 0
+
+
+@pytest.mark.parametrize("name", ["tiny", "mixed"])
+def test_dispatch_order_hint_does_not_change_results(name):
+    """Sequences dispatched longest-first (seq_order hint) or in natural order: bit-identical results."""
+    w = _workload(name)
+    a = DeviceWorkload(w, order_hints=True)
+    b = DeviceWorkload(w, order_hints=False)
+    for x, y in zip(a.results(), b.results()):
+        assert np.array_equal(x, y, equal_nan=True)
+    for x, y in zip(a.fused_results(), b.fused_results()):
+        assert np.array_equal(x, y, equal_nan=True)
