@@ -131,6 +131,16 @@ def _cpu_baseline(w, target_s):
             break
     per_step = el / reps
     kv = w.kv_bytes()
+    # One core: a prefix of the batch (whole sequences, all partitions), sized to about a tenth of target_s.
+    per_seq = per_step * threads / w.batch  # rough single-core seconds per sequence
+    n_single = int(max(1, min(w.batch, 0.1 * target_s / max(per_seq, 1e-9))))
+    seqs = list(range(n_single))
+    t_start = time.perf_counter()
+    o1, l1 = oracle.workload_partials(w, seqs=seqs, threads=1)
+    oracle.merge(o1, l1)
+    t1 = time.perf_counter() - t_start
+    n1 = n_single
+    kv1 = int(np.sum(w.kv_end[:, :n1].astype(np.int64) - w.kv_begin[:, :n1])) * w.num_kv_heads * 128 * 2 * 2
     model = ""
     try:
         for line in open("/proc/cpuinfo"):
@@ -149,6 +159,12 @@ def _cpu_baseline(w, target_s):
                   f"fp64, {reps} repetitions in {el:.1f} s",
         "cpu_model": model,
         "s_per_step": per_step,
+        "single_core": {
+            "value": kv1 / t1 / 1e9,
+            "unit": "GB/s",
+            "cores": 1,
+            "sample": f"first {n1} of {w.batch} sequences (all partitions + merge), fp64, {t1:.2f} s",
+        },
     }
 
 
@@ -202,6 +218,43 @@ def main():
     ms_per_step = wall * 1e3 / args.steps  # host wall clock, synchronised on both sides
     print(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step", file=sys.stderr, flush=True)
 
+    # Cold caches: the same step K times with events around each step alone and a 512 MiB
+    # scrub write between steps (outside the events), so neither L2 nor the last-level cache
+    # holds K/V from the previous step.
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    cold_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for k in range(args.steps):
+            scrub.fill_(k & 0xFF)
+            cold_ev[k][0].record(stream)
+            dw.step_on(h)
+            cold_ev[k][1].record(stream)
+    stream.synchronize()
+    cold_us = np.array([a.elapsed_time(b) * 1e3 for a, b in cold_ev])
+    del scrub
+
+    # Practical ceiling of the access pattern: the same K/V tiles read through the same
+    # table walk with no arithmetic (bana_debug_gather_read over all partitions).
+    from paper_2510_13223_amd import bana
+
+    sink = torch.empty((w.batch, w.num_kv_heads), dtype=torch.int32, device=dev)
+
+    def gather():
+        bana.bana_debug_gather_read(dw.k_cache, dw.v_cache, dw.block_table, dw.kv_begin, dw.kv_end, sink,
+                                    stream=stream)
+
+    for _ in range(args.warmup):
+        gather()
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for _ in range(args.steps):
+        gather()
+    torch.cuda.synchronize()
+    gather_s = (time.perf_counter() - wall0) / args.steps
+    print(f"[bench] gather-read ceiling: {gather_s * 1e6:.1f} us", file=sys.stderr, flush=True)
+
     # Timed region 2: the same K steps with HIP events around every partial-attention launch,
     # recorded on the stream the kernel runs on (event records add a little time between
     # kernels, so the step time above is taken without them).
@@ -230,7 +283,6 @@ def main():
     print(f"[bench] fused path: {fused_ms * 1e3:.1f} us/step", file=sys.stderr, flush=True)
 
     # Timed region 4: KV-block migration of the last (migrated) partition into a second pool.
-    from paper_2510_13223_amd import bana
 
     mig = workloads.make_migration(w, P - 1, seed=1)
     mig_blocks = int(np.sum(mig.blk_end - mig.blk_begin))
@@ -295,6 +347,23 @@ def main():
             "tokens_per_s": round(w.batch / (fused_ms / 1e3), 1),
         },
         "partial_kernels_kv_gbs": round(partial_kv_gbs, 2),
+        "cold_cache": {
+            "method": "events around each step alone, 512 MiB scrub write between steps",
+            "median_us": round(float(np.median(cold_us)), 2),
+            "p10_us": round(float(np.percentile(cold_us, 10)), 2),
+            "p90_us": round(float(np.percentile(cold_us, 90)), 2),
+            "value": round(kv_bytes / (float(np.median(cold_us)) / 1e6) / 1e9, 2),
+            "unit": "GB/s",
+        },
+        "gather_read_ceiling": {
+            "entry_point": "bana_debug_gather_read",
+            "what": "the step's K/V tiles read through the block table with the attention kernel's load shapes, "
+                    "no arithmetic",
+            "us": round(gather_s * 1e6, 2),
+            "value": round(kv_bytes / gather_s / 1e9, 2),
+            "unit": "GB/s",
+            "frac_of_hbm_peak": round(kv_bytes / gather_s / 1e9 / HBM_PEAK_GBS, 4),
+        },
         "migration": {
             "entry_point": "bana_migrate_kv_blocks",
             "partition": P - 1,

@@ -172,8 +172,9 @@ bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void
  * lse_out = -inf;  otherwise M = max_J lses[p][r], w_p = exp(lses[p][r] - M),
  *   out[r]     = sum_J w_p out_partials[p][r] / sum_J w_p,
  *   lse_out[r] = M + ln sum_J w_p.
- * Rows of parts with lse = -inf are never read.  Summation runs in an order
- * fixed by n_parts alone, so results are deterministic.
+ * Rows of parts with lse = -inf never enter a sum: they may hold anything,
+ * NaN included (they lie inside the buffer and may be loaded).  Summation
+ * runs in an order fixed by n_parts alone, so results are deterministic.
  * Of d, only batch, num_q_heads and head_dim are read.
  *   out_partials fp32 [n_parts][batch][num_q_heads][head_dim]
  *   lses         fp32 [n_parts][batch][num_q_heads]
@@ -254,6 +255,23 @@ const char* bana_last_error(void);
  */
 bana_status bana_debug_kv_rows(const bana_dims* d, const int32_t* block_table, const int32_t* kv_range_begin,
                                const int32_t* kv_range_end, int64_t* rows_out, void* stream);
+
+/*
+ * Measurement hook: the K/V read of attention over the ranges
+ * [kv_range_begin[p][b], kv_range_end[p][b]) (p < n_parts), with the same
+ * table walk and load shapes and no arithmetic, giving the practical
+ * bandwidth ceiling of that access pattern.  Every 4 KiB K and V tile of
+ * every covered block is read whole (a block covered by two ranges is read
+ * twice) and its 32-bit words are XOR-folded:
+ *   sink[b][g] = XOR of all 32-bit words of the K and V tiles of kv head g
+ *                of the covered blocks of sequence b
+ * so the result is checkable on the host.  sink: uint32 [batch][num_kv_heads]
+ * (device).  Ranges are preconditions as for the attention calls.  Errors as
+ * for the other calls; n_parts < 1 gives BANA_ERR_INVALID.
+ */
+bana_status bana_debug_gather_read(const bana_dims* d, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* kv_range_begin,
+                                   const int32_t* kv_range_end, int32_t n_parts, uint32_t* sink, void* stream);
 
 #ifdef __cplusplus
 }

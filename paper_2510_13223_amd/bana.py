@@ -89,6 +89,8 @@ def lib() -> ctypes.CDLL:
     L.bana_copy_async.restype = ctypes.c_int
     L.bana_debug_kv_rows.argtypes = [D, P, P, P, P, P]
     L.bana_debug_kv_rows.restype = ctypes.c_int
+    L.bana_debug_gather_read.argtypes = [D, P, P, P, P, P, ctypes.c_int32, P, P]
+    L.bana_debug_gather_read.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -310,3 +312,27 @@ def bana_debug_kv_rows(block_table, kv_range_begin, kv_range_end, num_blocks: in
                                   _ptr(rows_out), _stream(stream))
     if st != BANA_OK:
         raise BanaError(st, "bana_debug_kv_rows")
+
+
+def bana_debug_gather_read(k_cache, v_cache, block_table, kv_range_begin, kv_range_end, sink, stream=None) -> None:
+    """K/V read of the ranges ``[n_parts, B]`` with no arithmetic; ``sink`` uint32 as int32 [B, Hkv].
+
+    See ``bana_debug_gather_read`` in include/bana.h (sink[b][g] is the XOR of
+    the 32-bit words of every covered K and V tile of (b, g)).
+    """
+    nb, Hkv, D8, bs, _ = k_cache.shape
+    _need(k_cache, "k_cache", torch.bfloat16, (nb, Hkv, D8, bs, 8))
+    _need(v_cache, "v_cache", torch.bfloat16, (nb, Hkv, D8 * 8, bs))
+    _need(block_table, "block_table", torch.int32)
+    B, mb = block_table.shape
+    if kv_range_begin.dim() != 2 or kv_range_begin.shape[1] != B:
+        raise ValueError("kv_range_begin must be [n_parts, B]")
+    n = kv_range_begin.shape[0]
+    _need(kv_range_begin, "kv_range_begin", torch.int32, (n, B))
+    _need(kv_range_end, "kv_range_end", torch.int32, (n, B))
+    _need(sink, "sink", torch.int32, (B, Hkv))
+    dims = bana_dims(B, Hkv, Hkv, D8 * 8, bs, mb, nb, 0, 0, 0, 0, 0)
+    st = lib().bana_debug_gather_read(ctypes.byref(dims), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                      _ptr(kv_range_begin), _ptr(kv_range_end), n, _ptr(sink), _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_debug_gather_read")

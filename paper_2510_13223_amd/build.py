@@ -21,7 +21,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libbana.so")
-SOURCES = ["attn_partial.hip", "merge.hip", "migrate.hip", "validate.hip", "debug_rows.hip", "bana_api.cpp"]
+SOURCES = ["attn_partial.hip", "merge.hip", "migrate.hip", "validate.hip", "debug_rows.hip", "gather_read.hip",
+           "bana_api.cpp"]
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")

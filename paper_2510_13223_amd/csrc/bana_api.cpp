@@ -321,4 +321,18 @@ bana_status bana_debug_kv_rows(const bana_dims* d, const int32_t* block_table, c
                                                d->max_blocks_per_seq, rows_out, static_cast<hipStream_t>(stream)));
 }
 
+bana_status bana_debug_gather_read(const bana_dims* d, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* kv_range_begin,
+                                   const int32_t* kv_range_end, int32_t n_parts, uint32_t* sink, void* stream) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!k_cache || !v_cache || !block_table || !kv_range_begin || !kv_range_end || !sink || n_parts < 1)
+    return BANA_ERR_INVALID;
+  if (!aligned16(k_cache) || !aligned16(v_cache)) return BANA_ERR_INVALID;
+  if ((int64_t)d->batch * d->num_kv_heads > INT32_MAX) return BANA_ERR_UNSUPPORTED;  // one workgroup per (b, g)
+  return device_status(bana::launch_gather_read(k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts,
+                                                d->batch, d->num_kv_heads, d->max_blocks_per_seq, sink,
+                                                static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -48,6 +48,12 @@ hipError_t launch_validate(const int32_t* table, const int32_t* seq_lens, const 
                            int n_parts, int B, int max_blocks, int64_t num_blocks, int32_t* result,
                            hipStream_t stream);
 
+// K/V read of the attention ranges with no arithmetic (bandwidth ceiling of the access pattern);
+// sink[b * Hkv + g] = XOR of the 32-bit words read for (b, g).
+hipError_t launch_gather_read(const void* k, const void* v, const int32_t* table, const int32_t* begin,
+                              const int32_t* end, int n_parts, int B, int Hkv, int max_blocks, uint32_t* sink,
+                              hipStream_t stream);
+
 // Address export for the tests (rows of the K pool visited per logical token).
 hipError_t launch_debug_rows(const int32_t* table, const int32_t* begin, const int32_t* end, int B, int Hkv,
                              int max_blocks, int64_t* rows, hipStream_t stream);

@@ -525,3 +525,43 @@ def test_dispatch_order_hint_does_not_change_results(name):
         assert np.array_equal(x, y, equal_nan=True)
     for x, y in zip(a.fused_results(), b.fused_results()):
         assert np.array_equal(x, y, equal_nan=True)
+
+
+def _gather_xor_ref(w, begin, end):
+    """Host XOR of the 32-bit words of every covered K and V tile, per (sequence, kv head)."""
+    ref = np.zeros((w.batch, w.num_kv_heads), dtype=np.uint32)
+    for b in range(w.batch):
+        blks = []
+        for p in range(begin.shape[0]):
+            t0, t1 = int(begin[p, b]), int(end[p, b])
+            if t1 > t0:
+                blks.extend(int(w.block_table[b, j]) for j in range(t0 // 16, (t1 - 1) // 16 + 1))
+        if not blks:
+            continue
+        idx = np.array(blks, dtype=np.int64)
+        for g in range(w.num_kv_heads):
+            kw = np.ascontiguousarray(w.k_cache[idx, g]).reshape(len(idx), -1).view(np.uint32)
+            vw = np.ascontiguousarray(w.v_cache[idx, g]).reshape(len(idx), -1).view(np.uint32)
+            ref[b, g] = np.bitwise_xor.reduce(kw, axis=None) ^ np.bitwise_xor.reduce(vw, axis=None)
+    return ref
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_gather_read_covers_exactly_the_attention_tiles(seed):
+    w = _workload("tiny", seed)
+    _log(f"[gather] tiny seed={seed}")
+    dw = DeviceWorkload(w)
+    # The workload's partitions, plus an extra set: an empty range, a range inside one block,
+    # and a range that overlaps partition 0 (its shared blocks are read twice and cancel).
+    extra_b = np.zeros((3, w.batch), dtype=np.int32)
+    extra_e = np.zeros((3, w.batch), dtype=np.int32)
+    for b in range(w.batch):
+        L = int(w.seq_lens[b])
+        extra_b[1, b], extra_e[1, b] = 17, 20
+        extra_b[2, b], extra_e[2, b] = 5, min(L, 300)
+    for begin, end in ((w.kv_begin, w.kv_end), (extra_b, extra_e)):
+        sink = torch.zeros((w.batch, w.num_kv_heads), dtype=torch.int32, device="cuda")
+        bana.bana_debug_gather_read(dw.k_cache, dw.v_cache, dw.block_table, torch.from_numpy(begin).cuda(),
+                                    torch.from_numpy(end).cuda(), sink)
+        got = sink.cpu().numpy().view(np.uint32)
+        np.testing.assert_array_equal(got, _gather_xor_ref(w, begin, end))

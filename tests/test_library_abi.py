@@ -190,3 +190,17 @@ def test_workspace_sizing_follows_the_plan(lib):
     # an explicit chunk hint sizes the workspace exactly
     d = bana.make_dims(8, 32, 8, 8192, 50000, chunks_hint=4)
     assert lib.bana_decode_attn_workspace_bytes(ctypes.byref(d)) == (4 * 8 * 32 * 129 * 4 + 255) // 256 * 256
+
+
+def test_gather_read_rejects_bad_arguments(lib):
+    d = _dims()
+    args = [FAKE] * 5
+    assert lib.bana_debug_gather_read(ctypes.byref(d), *args, 0, FAKE, None) == -1
+    assert lib.bana_debug_gather_read(None, *args, 1, FAKE, None) == -1
+    for i in range(5):
+        a = list(args)
+        a[i] = None
+        assert lib.bana_debug_gather_read(ctypes.byref(d), *a, 1, FAKE, None) == -1, i
+    assert lib.bana_debug_gather_read(ctypes.byref(d), *args, 1, None, None) == -1
+    assert lib.bana_debug_gather_read(ctypes.byref(d), ctypes.c_void_p(0x100008), *args[1:], 1, FAKE, None) == -1
+    assert lib.bana_debug_gather_read(ctypes.byref(_dims(head_dim=64)), *args, 1, FAKE, None) == -2
