@@ -9,15 +9,21 @@
 // gives out = 0, lse_out = -inf.
 //
 // HBM-bound.  32 consecutive threads cover one 128-float row (16 bytes each,
-// one coalesced 512-byte access per part).  With many parts per row (the
-// chunk partials of a long range, or many migrated partitions) the parts of
-// a row are spread over KP thread groups that load independently, so the
-// merge is not a chain of dependent loads; the KP partial sums are added in
-// group order through LDS.  With at most four parts (the usual local +
-// migrated split) every lse and every partial row is loaded up front, before
-// any of them is used, so the kernel waits on one round of memory latency
-// instead of two.  The part-to-group assignment and every summation order
-// depend only on n_parts, so results are deterministic.
+// one coalesced 512-byte access per part).  Two kernels:
+//  * up to four parts (the usual local + migrated split): every lse and every
+//    partial row is loaded up front, before any of them is used, so the
+//    kernel waits on one round of memory latency;
+//  * more parts (many migrated partitions, or the chunk partials of long
+//    ranges): the 32 lanes of a row first read 32 parts' lse at once and
+//    reduce their max with lane shuffles, then stream the partial rows with
+//    loads that do not depend on any lse (the weights come from the lanes by
+//    shuffle), so loads of consecutive parts overlap.  With few rows the parts
+//    of a row are spread over KP thread groups; each group keeps its sums
+//    relative to its own max and the KP groups are combined through LDS,
+//    rescaled to the common max (the same log-sum-exp algebra once more).
+// The part-to-group assignment and every summation order depend only on
+// n_parts and the total row count, so results are deterministic, and a merge
+// restricted to a range of heads gives the same bits as the full merge.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -28,60 +34,6 @@ namespace bana {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-template <int KP>
-__global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ outs, const float* __restrict__ lses,
-                                                    int n_parts, int64_t B, int Hq, int h0, int hn,
-                                                    float* __restrict__ out, float* __restrict__ lse_out) {
-  constexpr int R = 256 / (32 * KP);  // rows per workgroup
-  __shared__ f32x4 sm_acc[KP > 1 ? R * KP * 32 : 1];
-  __shared__ float sm_w[KP > 1 ? R * KP : 1];
-  const int t = threadIdx.x;
-  const int d4 = t & 31;
-  const int k = (t >> 5) % KP;  // part group
-  const int rl = t / (32 * KP);
-  const int64_t r = (int64_t)blockIdx.x * R + rl;  // row among the B x hn merged rows
-  const int64_t rows = B * Hq;                      // row stride of one part
-  const bool live = r < B * hn;
-  const int64_t row = live ? (r / hn) * Hq + h0 + r % hn : 0;
-
-  float M = -INFINITY;
-  if (live)
-    for (int p = 0; p < n_parts; ++p) M = fmaxf(M, lses[(int64_t)p * rows + row]);
-  float wsum = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (live && M != -INFINITY) {
-    for (int p = k; p < n_parts; p += KP) {
-      const float l = lses[(int64_t)p * rows + row];
-      if (l == -INFINITY) continue;
-      const float w = expf(l - M);
-      wsum += w;
-      acc += w * reinterpret_cast<const f32x4*>(outs + ((int64_t)p * rows + row) * 128)[d4];
-    }
-  }
-  if (KP > 1) {
-    sm_acc[(rl * KP + k) * 32 + d4] = acc;
-    if (d4 == 0) sm_w[rl * KP + k] = wsum;
-    __syncthreads();
-    if (k != 0) return;
-    acc = f32x4{0.f, 0.f, 0.f, 0.f};
-    wsum = 0.f;
-#pragma unroll
-    for (int j = 0; j < KP; ++j) {
-      acc += sm_acc[(rl * KP + j) * 32 + d4];
-      wsum += sm_w[rl * KP + j];
-    }
-  }
-  if (!live) return;
-  f32x4* dst = reinterpret_cast<f32x4*>(out + row * 128) + d4;
-  if (M == -INFINITY) {
-    *dst = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (lse_out != nullptr && d4 == 0) lse_out[row] = -INFINITY;
-    return;
-  }
-  *dst = acc * (1.0f / wsum);
-  if (lse_out != nullptr && d4 == 0) lse_out[row] = M + logf(wsum);
-}
 
 // At most NP parts, all loaded before use.  Parts with lse = -inf are loaded
 // too (their rows lie inside the partial buffer) but never enter a sum.
@@ -129,14 +81,113 @@ __global__ __launch_bounds__(256) void merge_few_kernel(const float* __restrict_
   if (lse_out != nullptr && d4 == 0) lse_out[row] = M + logf(wsum);
 }
 
+constexpr int kUnroll = 4;  // partial rows in flight per lane
+
+// Any number of parts.  Group k (of KP) of a row takes parts k, k + KP, ...;
+// its q-th part is p = k + KP q.
 template <int KP>
-hipError_t launch(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn, float* out,
-                  float* lse_out, hipStream_t stream) {
+__global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict__ outs,
+                                                         const float* __restrict__ lses, int n_parts, int64_t B,
+                                                         int Hq, int h0, int hn, float* __restrict__ out,
+                                                         float* __restrict__ lse_out) {
+  constexpr int R = 256 / (32 * KP);  // rows per workgroup
+  __shared__ f32x4 sm_acc[KP > 1 ? R * KP * 32 : 1];
+  __shared__ float sm_m[KP > 1 ? R * KP : 1];
+  __shared__ float sm_w[KP > 1 ? R * KP : 1];
+  const int t = threadIdx.x;
+  const int d4 = t & 31;
+  const int k = (t >> 5) % KP;
+  const int rl = t / (32 * KP);
+  const int64_t r = (int64_t)blockIdx.x * R + rl;  // row among the B x hn merged rows
+  const int64_t rows = B * Hq;                      // row stride of one part
+  const bool live = r < B * hn;
+  const int64_t row = live ? (r / hn) * Hq + h0 + r % hn : 0;
+  const int nq = live && n_parts > k ? (n_parts - k + KP - 1) / KP : 0;
+  const int64_t lstride = (int64_t)KP * rows;                  // from the q-th part of the group to the next
+  const float* lrow = lses + (int64_t)k * rows + row;           // lse of the q-th part: lrow[q * lstride]
+  const float* orow = outs + ((int64_t)k * rows + row) * 128;  // its row: orow + q * lstride * 128
+
+  // Group max: lane d4 reads parts q = d4, d4 + 32, ...
+  float l0 = -INFINITY;
+  if (d4 < nq) l0 = lrow[d4 * lstride];
+  float m = l0;
+  for (int q = d4 + 32; q < nq; q += 32) m = fmaxf(m, lrow[q * lstride]);
+#pragma unroll
+  for (int off = 16; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 32));
+
+  float wsum = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (m != -INFINITY) {
+    for (int q0 = 0; q0 < nq; q0 += 32) {
+      // Weight of part q0 + d4 on lane d4 (0 past the end and for empty parts).
+      const float lq = q0 == 0 ? l0 : (q0 + d4 < nq ? lrow[(q0 + d4) * lstride] : -INFINITY);
+      const float wq = lq == -INFINITY ? 0.f : expf(lq - m);
+      const int n = min(32, nq - q0);
+      int j = 0;
+      for (; j + kUnroll <= n; j += kUnroll) {
+        f32x4 o[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+          o[u] = reinterpret_cast<const f32x4*>(orow + (q0 + j + u) * lstride * 128)[d4];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const float w = __shfl(wq, j + u, 32);
+          wsum += w;
+          if (w != 0.f) acc += w * o[u];
+        }
+      }
+      for (; j < n; ++j) {
+        const f32x4 o = reinterpret_cast<const f32x4*>(orow + (q0 + j) * lstride * 128)[d4];
+        const float w = __shfl(wq, j, 32);
+        wsum += w;
+        if (w != 0.f) acc += w * o;
+      }
+    }
+  }
+  float M = m;
+  if (KP > 1) {
+    sm_acc[(rl * KP + k) * 32 + d4] = acc;
+    if (d4 == 0) {
+      sm_m[rl * KP + k] = m;
+      sm_w[rl * KP + k] = wsum;
+    }
+    __syncthreads();
+    if (k != 0) return;
+    M = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < KP; ++j) M = fmaxf(M, sm_m[rl * KP + j]);
+    acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    wsum = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int j = 0; j < KP; ++j) {
+        const float mj = sm_m[rl * KP + j];
+        if (mj == -INFINITY) continue;
+        const float s = expf(mj - M);
+        acc += s * sm_acc[(rl * KP + j) * 32 + d4];
+        wsum += s * sm_w[rl * KP + j];
+      }
+    }
+  }
+  if (!live) return;
+  f32x4* dst = reinterpret_cast<f32x4*>(out + row * 128) + d4;
+  if (M == -INFINITY) {
+    *dst = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (lse_out != nullptr && d4 == 0) lse_out[row] = -INFINITY;
+    return;
+  }
+  *dst = acc * (1.0f / wsum);
+  if (lse_out != nullptr && d4 == 0) lse_out[row] = M + logf(wsum);
+}
+
+template <int KP>
+hipError_t launch_many(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn,
+                       float* out, float* lse_out, hipStream_t stream) {
   constexpr int R = 256 / (32 * KP);
   const int64_t rows = B * hn;
   const unsigned grid = (unsigned)((rows + R - 1) / R);
-  hipLaunchKernelGGL(merge_kernel<KP>, dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, B, Hq, h0, hn, out,
-                     lse_out);
+  hipLaunchKernelGGL(merge_many_kernel<KP>, dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, B, Hq, h0, hn,
+                     out, lse_out);
   return hipGetLastError();
 }
 
@@ -144,22 +195,22 @@ hipError_t launch(const float* outs, const float* lses, int n_parts, int64_t B, 
 
 hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn,
                         float* out, float* lse_out, hipStream_t stream) {
-  const int64_t rows = B * hn;
-  if (rows == 0) return hipSuccess;
+  if (B * hn == 0) return hipSuccess;
   if (n_parts <= 4) {
-    hipLaunchKernelGGL(merge_few_kernel<4>, dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, stream, outs, lses,
+    hipLaunchKernelGGL(merge_few_kernel<4>, dim3((unsigned)((B * hn + 7) / 8)), dim3(256), 0, stream, outs, lses,
                        n_parts, B, Hq, h0, hn, out, lse_out);
     return hipGetLastError();
   }
   // With enough rows to fill the GPU, one thread group per row streams best.
   // With few rows (long ranges of few sequences), spread a row's parts over
-  // up to 8 thread groups, at least 2 parts each.
-  if (rows < 4096) {
-    if (n_parts >= 16) return launch<8>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
-    if (n_parts >= 8) return launch<4>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
-    if (n_parts >= 4) return launch<2>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
+  // up to 8 thread groups, at least 4 parts each.  The choice uses the full
+  // row count B x Hq so that a head range merges exactly like the full call.
+  if (B * Hq < 4096) {
+    if (n_parts >= 32) return launch_many<8>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
+    if (n_parts >= 16) return launch_many<4>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
+    if (n_parts >= 8) return launch_many<2>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
   }
-  return launch<1>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
+  return launch_many<1>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
 }
 
 }  // namespace bana

@@ -281,13 +281,19 @@ def test_fused_dominant_key_and_all_empty():
     assert np.all(fo == 0.0) and np.all(np.isneginf(fl))
 
 
-def test_merge_matches_oracle_merge():
-    rng = np.random.default_rng(0)
-    n, B, Hq = 5, 7, 8
+# (parts, batch, heads): the few-part kernel, and the many-part kernel with 1, 2, 4 and 8 thread
+# groups per row, including more than 32 parts per group (several lse rounds per lane).
+@pytest.mark.parametrize("n,B,Hq", [(2, 7, 8), (4, 3, 8), (5, 7, 8), (9, 7, 8), (20, 3, 8), (70, 2, 8),
+                                    (300, 2, 8), (40, 128, 32), (6, 1, 1)])
+def test_merge_matches_oracle_merge(n, B, Hq):
+    rng = np.random.default_rng(n * 1000 + B)
     outs = rng.standard_normal((n, B, Hq, 128)).astype(np.float32)
     lses = (rng.standard_normal((n, B, Hq)) * 20).astype(np.float32)
     lses[rng.random((n, B, Hq)) < 0.3] = -np.inf
     lses[:, 0, 0] = -np.inf  # an all-empty row
+    if B * Hq > 1:
+        lses[: n // 2, -1, -1] = -np.inf  # a row whose first half of parts (whole thread groups) is empty
+        lses[n // 2:, -1, -1] = 80.0 * np.arange(n - n // 2)  # live parts far apart: most weights underflow
     outs[np.isneginf(lses)] = np.nan  # rows of empty parts are never read
     d_out = torch.empty((B, Hq, 128), dtype=torch.float32, device="cuda")
     d_lse = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
