@@ -23,8 +23,10 @@
  *  - Host-checkable argument errors return before any HIP call:
  *    BANA_ERR_INVALID for a NULL required pointer, a non-positive size,
  *    num_q_heads % num_kv_heads != 0, n_parts < 1 or a misaligned pointer;
- *    BANA_ERR_UNSUPPORTED for head_dim != 128, block_size != 16 or a GQA
- *    group (num_q_heads / num_kv_heads) above 16.
+ *    BANA_ERR_UNSUPPORTED for head_dim != 128, block_size != 16, a GQA
+ *    group (num_q_heads / num_kv_heads) above 16, or sizes whose indices
+ *    leave 32 bits (batch * max_blocks_per_seq, max_blocks_per_seq * 16 or
+ *    batch * num_q_heads above 2^31 - 1).
  *  - A failed launch returns BANA_ERR_DEVICE; bana_last_error() then holds
  *    the HIP error text (per calling thread).
  *  - Device-resident values are preconditions and are not checked per call:
@@ -85,7 +87,10 @@ typedef struct {
   int32_t max_range_tokens;   /* upper bound of kv_range_end - kv_range_begin over sequences */
   int32_t waves_hint;         /* waves per (sequence, kv head, chunk): 1, 2, 4 or 8 */
   int32_t chunks_hint;        /* chunks a range may be split into (needs workspace) */
-  int32_t reserved;           /* must be 0 */
+  int32_t plan_hint;          /* 0 = choose; 1 = chunked launch; 2 = balanced launch
+                                 (equal block intervals per wavefront across
+                                 sequences; needs workspace and batch <= 64,
+                                 otherwise the chunked launch runs) */
   int64_t total_range_tokens; /* sum over sequences of kv_range_end - kv_range_begin */
   /* Optional device array [batch]: the order in which sequences are
    * dispatched (a permutation of 0..batch-1; longest range first lets the
@@ -105,9 +110,14 @@ typedef struct {
  *
  * workspace: optional device scratch of workspace_bytes bytes, at least
  * bana_decode_attn_workspace_bytes(d) for ranges to be split across several
- * workgroups (long ranges, few sequences); with less (or NULL, 0) the call
- * runs unsplit, with the same results up to rounding order.  The contents
- * need no initialisation and are garbage afterwards.  Results are
+ * workgroups (long ranges, few sequences, or uneven lengths: with the range
+ * hints the library may cut the call's blocks into equal intervals across
+ * sequences, one per wavefront); with less (or NULL, 0) the call runs
+ * unsplit, with the same results up to rounding order.  The contents
+ * need no initialisation and are garbage afterwards.  Calls that may run at
+ * the same time (on different streams without an event between them) must
+ * not share a workspace: they would overwrite each other's partials and
+ * give wrong results (never an access outside the caller's buffers).  Results are
  * bit-identical run to run for the same inputs and dims, and invariant to
  * the physical placement of blocks.
  */

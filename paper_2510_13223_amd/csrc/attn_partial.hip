@@ -10,15 +10,27 @@
 // algebra as the final O = O^(1) + O^(2)), computed in one launch.
 //
 // Work decomposition.  The blocks of a sequence's ranges are concatenated
-// into one virtual block sequence.  One workgroup per (chunk c, sequence b,
-// kv head g), linearised chunk-major so that every (b, g) has its first
-// chunk in the first wave of dispatch.  A workgroup of W wavefronts walks the
-// virtual blocks of its chunk round-robin (block jr goes to wave jr % W),
-// mapping each to (range, logical block) with a segment cursor; each wavefront keeps
-// an online-softmax state for all G query heads of the kv head, and the W
-// states are combined through LDS at the end.  A range longer than one chunk
-// leaves one partial per chunk in caller workspace, merged by the merge
-// kernel with the same log-sum-exp algebra as the partition merge.
+// into one virtual block sequence, mapped back to (range, logical block) by
+// a segment cursor.  Two launch shapes:
+//  * chunked: one workgroup per (chunk c, sequence b, kv head g),
+//    linearised chunk-major so that every (b, g) has its first chunk in the
+//    first wave of dispatch.  A workgroup of W wavefronts walks the virtual
+//    blocks of its chunk round-robin (block jr goes to wave jr % W); each
+//    wavefront keeps an online-softmax state for all G query heads of the
+//    kv head, and the W states are combined through LDS at the end.  A range
+//    longer than one chunk leaves one partial per chunk in caller workspace,
+//    merged by the merge kernel with the same log-sum-exp algebra as the
+//    partition merge.
+//  * balanced (uneven ranges of few sequences): the virtual blocks of all
+//    sequences, in sequence order, form one list per kv head, cut into K
+//    equal intervals of S = ceil(U / K) blocks (U = blocks of the whole call),
+//    one per wavefront.  A wavefront walks its interval block by block,
+//    leaving one partial per sequence piece it covers in workspace slot
+//    (k + b), which is unique (an interval and a sequence that overlap bound
+//    each other's position); the merge finds a sequence's pieces from the
+//    prefix sums of the block counts.  Every wavefront gets the same number of
+//    blocks whatever the lengths, so one long range no longer sets the time
+//    of the launch, and no range has to be rounded to whole chunks.
 //
 // One KV block (16 tokens x 128 dims for one kv head) per wavefront step:
 //   scores  S^T[16 tok x 16 col] = K[16 tok x 128] . Q^T[128 x 16 col]
@@ -107,89 +119,47 @@ __device__ __forceinline__ void load_v(u32x2 (&vr)[kDimTiles], const uint16_t* _
   for (int dt = 0; dt < kDimTiles; ++dt) vr[dt] = __builtin_nontemporal_load(src + 4 * 16 * dt);
 }
 
-template <int W>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) void partial_attn_kernel(PartialArgs a) {
-  extern __shared__ float smem[];
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  const int col = lane & 15;  // query head in group (score/output column); token row for K; dim for V
-  const int quad = lane >> 4;
-
-  int wg = blockIdx.x;
-  const int g = a.g0 + wg % a.ng;
-  wg /= a.ng;
-  const int b = a.seq_order != nullptr ? table_lookup(a.seq_order, 0, 0, wg % a.B) : wg % a.B;
-  const int c = wg / a.B;
-  const int G = a.G;
-  const int hq0 = g * G;
-
-  // The ranges ("segments") of this sequence: one per partition.  Lane p
-  // describes segment p; the segments' blocks are concatenated into one
-  // virtual block sequence [0, nblk) that the workgroup's chunks cut up.
-  int s_t0 = 0, s_t1 = 0, s_jfirst = 0, s_nblk = 0;
-  if (lane < a.n_parts) {
-    s_t0 = a.begin[(int64_t)lane * a.B + b];
-    s_t1 = a.end[(int64_t)lane * a.B + b];
-    if (s_t1 > s_t0) {
-      s_jfirst = s_t0 >> 4;
-      s_nblk = ((s_t1 - 1) >> 4) - s_jfirst + 1;
-    }
-  }
-  int s_vend = s_nblk;  // inclusive prefix sum over segments
+// B operand of the score product: Q^T, lane (col, quad) holds dims 32kk + 8quad + [0, 8)
+// of head hq0 + col (zero for col >= G).
+__device__ __forceinline__ void load_q(bf16x8 (&qop)[4], const uint16_t* __restrict__ q, int64_t row0, int col,
+                                       int quad, int G) {
+  const uint16_t* qrow = q + (row0 + (col < G ? col : 0)) * kHeadDim + 8 * quad;
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(s_vend, off);
-    if (lane >= off) s_vend += y;
+  for (int kk = 0; kk < 4; ++kk) {
+    u32x4 v = *reinterpret_cast<const u32x4*>(qrow + 32 * kk);
+    if (col >= G) v = u32x4{0u, 0u, 0u, 0u};
+    qop[kk] = __builtin_bit_cast(bf16x8, v);
   }
-  const int nblk = __builtin_amdgcn_readlane(s_vend, a.n_parts - 1);
-  int per = (nblk + a.nc - 1) / a.nc;
-  if (per < a.cmin) per = a.cmin;
-  const int nch = nblk > 0 ? (nblk + per - 1) / per : 0;
+}
 
-  // Destination of this workgroup's result.
-  const int64_t row0 = ((int64_t)(a.nc == 1 ? 0 : c) * a.B + b) * a.Hq + hq0;
-  float* __restrict__ out_dst = a.out + row0 * kHeadDim;
-  float* __restrict__ lse_dst = a.lse + row0;
-
-  if (c >= nch) {  // empty range or chunk: out = 0, lse = -inf (chunk slots only need the lse)
-    if (a.nc == 1) {
-      for (int i = threadIdx.x; i < G * (kHeadDim / 4); i += 64 * W)
-        reinterpret_cast<f32x4*>(out_dst)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    for (int i = threadIdx.x; i < G; i += 64 * W) lse_dst[i] = -INFINITY;
-    return;
-  }
-  const int jb0 = c * per;
-  const int jb1 = min(nblk, jb0 + per);
-
-  // B operand of the score product: Q^T, lane (col, quad) holds dims 32kk + 8quad + [0, 8) of head col.
-  bf16x8 qop[4];
-  {
-    const uint16_t* qrow = a.q + ((int64_t)b * a.Hq + hq0 + (col < G ? col : 0)) * kHeadDim + 8 * quad;
+// Scores of one block: s[i] = q(head col) . k(token slot 4*quad + i).
+__device__ __forceinline__ f32x4 block_scores(const bf16x8 (&qop)[4], const u32x4 (&kr)[4]) {
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      u32x4 v = *reinterpret_cast<const u32x4*>(qrow + 32 * kk);
-      if (col >= G) v = u32x4{0u, 0u, 0u, 0u};
-      qop[kk] = __builtin_bit_cast(bf16x8, v);
-    }
-  }
+  for (int kk = 0; kk < 4; ++kk)
+    s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[kk]), qop[kk], s, 0, 0, 0);
+  return s;
+}
 
+// Online-softmax state of one wavefront: acc[dt][i] = unnormalised output for
+// dim 16dt + 4quad + i of head col; m = running max; lsum = this lane's share
+// of the running sum (its token rows only, summed over the column at the end).
+struct Online {
   f32x4 acc[kDimTiles];
-#pragma unroll
-  for (int dt = 0; dt < kDimTiles; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m = -INFINITY;
-  float lsum = 0.f;
+  float m;
+  float lsum;
 
-  // Scores of one block: s[i] = q(head col) . k(token slot 4*quad + i).
-  auto scores = [&](const u32x4 (&kr)[4]) {
-    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+  __device__ __forceinline__ void init() {
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-      s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[kk]), qop[kk], s, 0, 0, 0);
-    return s;
-  };
-  // Online-softmax update and value accumulation of one block.
-  auto update = [&](f32x4 s, u32x2 (&vr)[kDimTiles], const int j, const int t0, const int t1) {
+    for (int dt = 0; dt < kDimTiles; ++dt) acc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m = -INFINITY;
+    lsum = 0.f;
+  }
+
+  // Online-softmax update and value accumulation of logical block j of a
+  // range [t0, t1) (j overlaps the range).
+  __device__ __forceinline__ void update(f32x4 s, u32x2 (&vr)[kDimTiles], const int j, const int t0, const int t1,
+                                         const int quad) {
     if (j * kBlockSize < t0 || j * kBlockSize + kBlockSize > t1) {  // partly covered block (wave-uniform)
       const int tok = j * kBlockSize + 4 * quad;
       const bool ok0 = tok + 0 >= t0 && tok + 0 < t1;
@@ -232,94 +202,175 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
       t = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, phi, t, 0, 0, 0);
       acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, plo, t, 0, 0, 0);
     }
-  };
-
-  // Software pipeline over this wave's blocks, one register set each for K
-  // and V: the next block's K is requested as soon as the score product has
-  // consumed the current one, and the next V as soon as the value product
-  // has consumed the current one, so about one block (8 KiB) per wave stays
-  // in flight through the softmax and MFMA work.  Table entries are read two
-  // blocks ahead with scalar loads.
-  // Cursor over the segments (wave-uniform): the segment holding virtual
-  // block v, advanced monotonically with readlane from the segment lanes.
-  struct Seg {
-    int p, vstart, vend, jfirst, t0, t1;
-  };
-  auto seg_at = [&](int p) {
-    Seg sg;
-    sg.p = p;
-    sg.vend = __builtin_amdgcn_readlane(s_vend, p);
-    sg.vstart = sg.vend - __builtin_amdgcn_readlane(s_nblk, p);
-    sg.jfirst = __builtin_amdgcn_readlane(s_jfirst, p);
-    sg.t0 = __builtin_amdgcn_readlane(s_t0, p);
-    sg.t1 = __builtin_amdgcn_readlane(s_t1, p);
-    return sg;
-  };
-  auto seek = [&](Seg& sg, int v) {
-    while (v >= sg.vend && sg.p + 1 < a.n_parts) sg = seg_at(sg.p + 1);
-  };
-
-  int jr = jb0 + wave;  // virtual block index
-  if (jr < jb1) {
-    const int vlast = jb1 - 1;
-    Seg cm = seg_at(0);  // segment of the block being computed
-    Seg ct = cm;         // segment of the block whose table entry is read
-    auto table_at = [&](int v) {
-      seek(ct, v);
-      return table_lookup(a.table, a.max_blocks, b, ct.jfirst + (v - ct.vstart));
-    };
-    const int32_t blk_first = table_at(jr);
-    int32_t blk_next = table_at(min(jr + W, vlast));
-    u32x4 kr[4];
-    u32x2 vr[kDimTiles];
-    {
-      const int64_t tile = kv_tile(blk_first, g, a.Hkv);
-      load_k(kr, a.k, tile, col, quad);
-      load_v(vr, a.v, tile, col, quad);
-    }
-    // Every load inside the loop is unconditional (the last block is peeled),
-    // so the in-order memory counter lets each wait cover exactly the tile
-    // it needs while the other one stays in flight.
-    while (jr + W < jb1) {
-      const int32_t blk_after = table_at(min(jr + 2 * W, vlast));
-      const int64_t tile_next = kv_tile(blk_next, g, a.Hkv);
-      const f32x4 s = scores(kr);
-      load_k(kr, a.k, tile_next, col, quad);
-      seek(cm, jr);
-      update(s, vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1);
-      load_v(vr, a.v, tile_next, col, quad);
-      jr += W;
-      blk_next = blk_after;
-    }
-    seek(cm, jr);
-    update(scores(kr), vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1);
   }
-  // acc[dt][i] = unnormalised output for dim 16dt + 4quad + i, head col; the
-  // per-lane lsum covers this lane's token rows only.
-  lsum = column_sum(lsum);
 
-  if (W == 1) {
+  // Normalised rows of the G heads (out_dst row = head in group) and their lse.
+  __device__ __forceinline__ void emit(float* __restrict__ out_dst, float* __restrict__ lse_dst, int col, int quad,
+                                       int G) {
+    const float l = column_sum(lsum);
     if (col < G) {
-      const float inv = 1.0f / lsum;
+      const float inv = 1.0f / l;
 #pragma unroll
       for (int dt = 0; dt < kDimTiles; ++dt)
         *reinterpret_cast<f32x4*>(out_dst + col * kHeadDim + 16 * dt + 4 * quad) = acc[dt] * inv;
-      if (quad == 0) lse_dst[col] = m + logf(lsum);
+      if (quad == 0) lse_dst[col] = m + logf(l);
     }
+  }
+};
+
+// The ranges ("segments") of one sequence, one per lane p < n_parts, with
+// the inclusive prefix sum of their block counts: the segments' blocks,
+// concatenated, are the sequence's virtual block sequence [0, nblk).
+struct Segments {
+  int t0, t1, jfirst, nblk, vend;
+
+  __device__ __forceinline__ void load(const PartialArgs& a, int b, int lane) {
+    t0 = t1 = jfirst = nblk = 0;
+    if (lane < a.n_parts) {
+      t0 = a.begin[(int64_t)lane * a.B + b];
+      t1 = a.end[(int64_t)lane * a.B + b];
+      if (t1 > t0) {
+        jfirst = t0 >> 4;
+        nblk = ((t1 - 1) >> 4) - jfirst + 1;
+      }
+    }
+    vend = nblk;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(vend, off);
+      if (lane >= off) vend += y;
+    }
+  }
+  __device__ __forceinline__ int total(int n_parts) const { return __builtin_amdgcn_readlane(vend, n_parts - 1); }
+};
+
+// Cursor over the segments (wave-uniform): the segment holding virtual block
+// v, advanced monotonically with readlane from the segment lanes.
+struct Seg {
+  int p, vstart, vend, jfirst, t0, t1;
+};
+
+__device__ __forceinline__ Seg seg_at(const Segments& sg, int p) {
+  Seg c;
+  c.p = p;
+  c.vend = __builtin_amdgcn_readlane(sg.vend, p);
+  c.vstart = c.vend - __builtin_amdgcn_readlane(sg.nblk, p);
+  c.jfirst = __builtin_amdgcn_readlane(sg.jfirst, p);
+  c.t0 = __builtin_amdgcn_readlane(sg.t0, p);
+  c.t1 = __builtin_amdgcn_readlane(sg.t1, p);
+  return c;
+}
+
+__device__ __forceinline__ void seek(const Segments& sg, Seg& c, int v, int n_parts) {
+  while (v >= c.vend && c.p + 1 < n_parts) c = seg_at(sg, c.p + 1);
+}
+
+// Software pipeline over the virtual blocks jr, jr + STEP, ... < jb1 of
+// sequence b, kv head g, one register set each for K and V: the next block's
+// K is requested as soon as the score product has consumed the current one,
+// and the next V as soon as the value product has consumed the current one,
+// so about one block (8 KiB) per wave stays in flight through the softmax and
+// MFMA work.  Table entries are read two blocks ahead with scalar loads.
+template <int STEP>
+__device__ __forceinline__ void walk_blocks(Online& st, const bf16x8 (&qop)[4], const Segments& sg,
+                                            const PartialArgs& a, int b, int g, int col, int quad, int jr, int jb1) {
+  if (jr >= jb1) return;
+  const int vlast = jb1 - 1;
+  Seg cm = seg_at(sg, 0);  // segment of the block being computed
+  Seg ct = cm;             // segment of the block whose table entry is read
+  auto table_at = [&](int v) {
+    seek(sg, ct, v, a.n_parts);
+    return table_lookup(a.table, a.max_blocks, b, ct.jfirst + (v - ct.vstart));
+  };
+  const int32_t blk_first = table_at(jr);
+  int32_t blk_next = table_at(min(jr + STEP, vlast));
+  u32x4 kr[4];
+  u32x2 vr[kDimTiles];
+  {
+    const int64_t tile = kv_tile(blk_first, g, a.Hkv);
+    load_k(kr, a.k, tile, col, quad);
+    load_v(vr, a.v, tile, col, quad);
+  }
+  // Every load inside the loop is unconditional (the last block is peeled),
+  // so the in-order memory counter lets each wait cover exactly the tile
+  // it needs while the other one stays in flight.
+  while (jr + STEP < jb1) {
+    const int32_t blk_after = table_at(min(jr + 2 * STEP, vlast));
+    const int64_t tile_next = kv_tile(blk_next, g, a.Hkv);
+    const f32x4 s = block_scores(qop, kr);
+    load_k(kr, a.k, tile_next, col, quad);
+    seek(sg, cm, jr, a.n_parts);
+    st.update(s, vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1, quad);
+    load_v(vr, a.v, tile_next, col, quad);
+    jr += STEP;
+    blk_next = blk_after;
+  }
+  seek(sg, cm, jr, a.n_parts);
+  st.update(block_scores(qop, kr), vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1, quad);
+}
+
+template <int W>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) void partial_attn_kernel(PartialArgs a) {
+  extern __shared__ float smem[];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int col = lane & 15;  // query head in group (score/output column); token row for K; dim for V
+  const int quad = lane >> 4;
+
+  int wg = blockIdx.x;
+  const int g = a.g0 + wg % a.ng;
+  wg /= a.ng;
+  const int b = a.seq_order != nullptr ? table_lookup(a.seq_order, 0, 0, wg % a.B) : wg % a.B;
+  const int c = wg / a.B;
+  const int G = a.G;
+  const int hq0 = g * G;
+
+  Segments sg;
+  sg.load(a, b, lane);
+  const int nblk = sg.total(a.n_parts);
+  int per = (nblk + a.nc - 1) / a.nc;
+  if (per < a.cmin) per = a.cmin;
+  const int nch = nblk > 0 ? (nblk + per - 1) / per : 0;
+
+  // Destination of this workgroup's result.
+  const int64_t row0 = ((int64_t)(a.nc == 1 ? 0 : c) * a.B + b) * a.Hq + hq0;
+  float* __restrict__ out_dst = a.out + row0 * kHeadDim;
+  float* __restrict__ lse_dst = a.lse + row0;
+
+  if (c >= nch) {  // empty range or chunk: out = 0, lse = -inf (chunk slots only need the lse)
+    if (a.nc == 1) {
+      for (int i = threadIdx.x; i < G * (kHeadDim / 4); i += 64 * W)
+        reinterpret_cast<f32x4*>(out_dst)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int i = threadIdx.x; i < G; i += 64 * W) lse_dst[i] = -INFINITY;
+    return;
+  }
+  const int jb0 = c * per;
+  const int jb1 = min(nblk, jb0 + per);
+
+  bf16x8 qop[4];
+  load_q(qop, a.q, (int64_t)b * a.Hq + hq0, col, quad, G);
+  Online st;
+  st.init();
+  walk_blocks<W>(st, qop, sg, a, b, g, col, quad, jb0 + wave, jb1);
+
+  if (W == 1) {
+    st.emit(out_dst, lse_dst, col, quad, G);
     return;
   }
 
+  const float lsum = column_sum(st.lsum);
   float* sm_m = smem;               // [W][16]
   float* sm_l = smem + 16 * W;      // [W][16]
   float* sm_acc = smem + 32 * W;    // [W][G][kRowPad]
   if (quad == 0) {
-    sm_m[wave * 16 + col] = m;      // -inf for a wave that saw no block
+    sm_m[wave * 16 + col] = st.m;   // -inf for a wave that saw no block
     sm_l[wave * 16 + col] = lsum;
   }
   if (col < G) {
 #pragma unroll
     for (int dt = 0; dt < kDimTiles; ++dt)
-      *reinterpret_cast<f32x4*>(sm_acc + (wave * G + col) * kRowPad + 16 * dt + 4 * quad) = acc[dt];
+      *reinterpret_cast<f32x4*>(sm_acc + (wave * G + col) * kRowPad + 16 * dt + 4 * quad) = st.acc[dt];
   }
   __syncthreads();
   for (int idx = threadIdx.x; idx < G * (kHeadDim / 4); idx += 64 * W) {
@@ -343,6 +394,70 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   }
 }
 
+// Balanced launch (batch <= 64): wavefront k of kv head g walks the blocks
+// [k S, (k + 1) S) (clipped to U) of the call's virtual block list and leaves
+// one partial per sequence piece in slot k + b of the piece buffers
+// ([slot][Hq][128] and [slot][Hq]).  Every wavefront computes the schedule
+// itself, one sequence per lane: block counts N_b, their prefix sums by lane
+// shuffles, U and S; the sequence holding block pos is the number of
+// sequences whose blocks end at or before pos.  The first wavefront of the
+// call also stores the prefix sums (prefix[0..B]) for the merge.
+template <int W>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) void balanced_attn_kernel(
+    PartialArgs a, int32_t* __restrict__ prefix, int K) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15;
+  const int quad = lane >> 4;
+  const int g = a.g0 + (int)(blockIdx.x % (unsigned)a.ng);
+  const int k = (int)(blockIdx.x / (unsigned)a.ng) * W + wave;
+  if (k >= K) return;
+  const int G = a.G;
+  const int hq0 = g * G;
+
+  int n_lane = 0;  // blocks of sequence `lane` over all its ranges
+  if (lane < a.B) {
+    for (int p = 0; p < a.n_parts; ++p) {
+      const int t0 = a.begin[(int64_t)p * a.B + lane];
+      const int t1 = a.end[(int64_t)p * a.B + lane];
+      if (t1 > t0) n_lane += ((t1 - 1) >> 4) - (t0 >> 4) + 1;
+    }
+  }
+  int incl = n_lane;  // blocks of sequences 0..lane
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off);
+    if (lane >= off) incl += y;
+  }
+  if (k == 0 && g == a.g0) {
+    if (lane < a.B) prefix[lane + 1] = incl;
+    if (lane == 0) prefix[0] = 0;
+  }
+  const int U = __builtin_amdgcn_readlane(incl, a.B - 1);
+  const int64_t S = U > K ? ((int64_t)U + K - 1) / K : 1;
+  const int u1 = (int)min((int64_t)U, (k + 1) * S);
+  int pos = (int)min((int64_t)U, k * S);
+
+  while (pos < u1) {
+    const int b = __builtin_popcountll(__ballot(lane < a.B && incl <= pos));  // sequence holding block pos
+    const int pb = b > 0 ? __builtin_amdgcn_readlane(incl, b - 1) : 0;
+    Segments sg;
+    sg.load(a, b, lane);
+    const int nb = sg.total(a.n_parts);
+    const int v0 = pos - pb;
+    const int v1 = min(u1 - pb, nb);
+
+    bf16x8 qop[4];
+    load_q(qop, a.q, (int64_t)b * a.Hq + hq0, col, quad, G);
+    Online st;
+    st.init();
+    walk_blocks<1>(st, qop, sg, a, b, g, col, quad, v0, v1);
+    const int64_t row0 = (int64_t)(k + b) * a.Hq + hq0;
+    st.emit(a.out + row0 * kHeadDim, a.lse + row0, col, quad, G);
+    pos = pb + v1;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stream) {
@@ -355,6 +470,13 @@ hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stre
     case 8: hipLaunchKernelGGL(partial_attn_kernel<8>, dim3(nwg), dim3(512), smem, stream, a); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_balanced_attn(const PartialArgs& a, int32_t* prefix, int K, hipStream_t stream) {
+  const unsigned nwg = (unsigned)((K + kBalancedWaves - 1) / kBalancedWaves) * (unsigned)a.ng;
+  hipLaunchKernelGGL(balanced_attn_kernel<kBalancedWaves>, dim3(nwg), dim3(64 * kBalancedWaves), 0, stream, a,
+                     prefix, K);
   return hipGetLastError();
 }
 

@@ -35,23 +35,28 @@ bana_status check_dims(const bana_dims* d) {
       d->max_blocks_per_seq <= 0 || d->num_blocks <= 0)
     return BANA_ERR_INVALID;
   if (d->num_q_heads % d->num_kv_heads != 0) return BANA_ERR_INVALID;
-  if (d->max_range_tokens < 0 || d->chunks_hint < 0 || d->reserved != 0 || d->total_range_tokens < 0)
+  if (d->max_range_tokens < 0 || d->chunks_hint < 0 || d->plan_hint < 0 || d->plan_hint > 2 ||
+      d->total_range_tokens < 0)
     return BANA_ERR_INVALID;
   if (d->waves_hint != 0 && d->waves_hint != 1 && d->waves_hint != 2 && d->waves_hint != 4 && d->waves_hint != 8)
     return BANA_ERR_INVALID;
   if (d->head_dim != kHeadDim || d->block_size != kBlockSize) return BANA_ERR_UNSUPPORTED;
   if (d->num_q_heads / d->num_kv_heads > kMaxGroup) return BANA_ERR_UNSUPPORTED;
-  // Index arithmetic of the kernels: table rows and token indices are 32-bit.
+  // Index arithmetic of the kernels: table rows, token indices, workgroup
+  // indices (one per sequence and kv head at least) and output rows are 32-bit.
   if ((int64_t)d->batch * d->max_blocks_per_seq > INT32_MAX ||
-      (int64_t)d->max_blocks_per_seq * kBlockSize > INT32_MAX)
+      (int64_t)d->max_blocks_per_seq * kBlockSize > INT32_MAX ||
+      (int64_t)d->batch * d->num_q_heads > INT32_MAX)
     return BANA_ERR_UNSUPPORTED;
   return BANA_OK;
 }
 
 struct Plan {
-  int waves;  // wavefronts per workgroup
-  int nc;     // chunks per (sequence, kv head)
-  int cmin;   // minimum blocks per chunk
+  int waves;      // wavefronts per workgroup
+  int nc;         // chunks per (sequence, kv head)
+  int cmin;       // minimum blocks per chunk
+  bool balanced;  // equal block intervals per wavefront across sequences
+  int K;          // balanced: wavefronts per kv head
 };
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
@@ -70,6 +75,16 @@ int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 //    twice the even share, into chunks of twice the even share.
 // Chunks need workspace; without it the call runs unsplit.  Without hints
 // the table width bounds the range length.
+//
+// Balanced launch (batch <= 64): one round of wavefronts per kv head, each
+// over an equal interval of the call's blocks in sequence order, the pieces
+// of a sequence merged afterwards.  Chosen when the longest hinted range
+// exceeds 1.5 x the mean, the (sequence, kv head) pairs cannot fill one round
+// and the call has at least kMinBlocksPerWave blocks per wavefront (or asked
+// for by plan_hint 2): that is where the chunked plan has to round every
+// range to whole chunks within a single round.  With a milder spread that
+// rounding costs less than the piece merge, and with many pairs several
+// dispatch rounds, longest range first, balance by themselves.
 Plan make_plan(const bana_dims* d) {
   const int64_t pairs = (int64_t)d->batch * d->num_kv_heads;
   int64_t bound = d->max_blocks_per_seq;  // blocks of the longest range
@@ -82,6 +97,21 @@ Plan make_plan(const bana_dims* d) {
       hinted ? std::max<int64_t>(1, d->total_range_tokens / (kBlockSize * (int64_t)d->batch) + 1) : bound;
   const bool uneven = hinted && 4 * bound > 5 * mean_blocks;
   Plan p;
+  p.balanced = false;
+  p.K = std::max(1, kTargetWaves / (bana::kBalancedWaves * d->num_kv_heads)) * bana::kBalancedWaves;
+  if (d->batch <= bana::kMaxBalancedBatch && d->waves_hint == 0 && d->chunks_hint == 0 && d->plan_hint != 1) {
+    const int64_t call_blocks = hinted ? d->total_range_tokens / kBlockSize + d->batch : 0;
+    const bool few_pairs = pairs < kTargetWaves / bana::kBalancedWaves;
+    const bool very_uneven = hinted && 2 * bound > 3 * mean_blocks;  // longest range > 1.5 x mean
+    p.balanced =
+        d->plan_hint == 2 || (very_uneven && few_pairs && call_blocks >= (int64_t)kMinBlocksPerWave * p.K);
+  }
+  if (p.balanced) {
+    p.waves = bana::kBalancedWaves;
+    p.nc = 1;
+    p.cmin = 1;
+    return p;
+  }
   if (d->waves_hint > 0)
     p.waves = d->waves_hint;
   else if (uneven && bound >= 8 * kMinBlocksPerWave)
@@ -121,12 +151,31 @@ Plan make_plan(const bana_dims* d) {
   return p;
 }
 
-size_t workspace_for(const bana_dims* d, int nc) {
-  if (nc <= 1) return 0;
-  const size_t rows = (size_t)nc * d->batch * d->num_q_heads;
-  const size_t bytes = rows * kHeadDim * sizeof(float) + rows * sizeof(float);
-  return (bytes + 255) & ~(size_t)255;
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace regions of a plan.  Chunked: chunk partials [nc][B][Hq][128] and
+// [nc][B][Hq].  Balanced: piece partials [K + B][Hq][128] and [K + B][Hq],
+// then the block-count prefix sums [B + 1].
+struct WorkspaceLayout {
+  size_t out, lse, prefix, total;
+};
+
+WorkspaceLayout layout_for(const bana_dims* d, const Plan& p) {
+  WorkspaceLayout w{0, 0, 0, 0};
+  size_t rows;
+  if (p.balanced) rows = ((size_t)p.K + d->batch) * d->num_q_heads;
+  else if (p.nc > 1) rows = (size_t)p.nc * d->batch * d->num_q_heads;
+  else return w;
+  w.lse = align256(rows * kHeadDim * sizeof(float));
+  w.total = align256(w.lse + rows * sizeof(float));
+  if (p.balanced) {
+    w.prefix = w.total;
+    w.total = align256(w.prefix + ((size_t)d->batch + 1) * sizeof(int32_t));
+  }
+  return w;
 }
+
+size_t workspace_for(const bana_dims* d, const Plan& p) { return layout_for(d, p).total; }
 
 bana_status device_status(hipError_t e) {
   if (e == hipSuccess) return BANA_OK;
@@ -152,7 +201,7 @@ const char* bana_last_error(void) { return g_last_error.c_str(); }
 
 size_t bana_decode_attn_workspace_bytes(const bana_dims* d) {
   if (check_dims(d) != BANA_OK) return 0;
-  return workspace_for(d, make_plan(d).nc);
+  return workspace_for(d, make_plan(d));
 }
 
 }  // extern "C"
@@ -168,8 +217,15 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
                           int n_parts, int g0, int ng, float* out, float* lse, void* workspace,
                           size_t workspace_bytes, void* stream) {
   Plan plan = make_plan(d);
-  const size_t need = workspace_for(d, plan.nc);
-  if (plan.nc > 1 && (workspace == nullptr || workspace_bytes < need)) plan.nc = 1;
+  const WorkspaceLayout ws = layout_for(d, plan);
+  if (ws.total > 0 && (workspace == nullptr || workspace_bytes < ws.total)) {
+    if (plan.balanced) {  // the chunked plan's launch shape, unsplit
+      bana_dims chunked = *d;
+      chunked.plan_hint = 1;
+      plan = make_plan(&chunked);
+    }
+    plan.nc = 1;
+  }
 
   bana::PartialArgs a;
   a.q = static_cast<const uint16_t*>(q);
@@ -191,6 +247,18 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
   a.cmin = plan.cmin;
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t rows = (int64_t)d->batch * d->num_q_heads;
+  if (plan.balanced) {
+    char* base = static_cast<char*>(workspace);
+    float* ws_out = reinterpret_cast<float*>(base + ws.out);
+    float* ws_lse = reinterpret_cast<float*>(base + ws.lse);
+    int32_t* prefix = reinterpret_cast<int32_t*>(base + ws.prefix);
+    a.out = ws_out;
+    a.lse = ws_lse;
+    hipError_t e = bana::launch_balanced_attn(a, prefix, plan.K, s);
+    if (e != hipSuccess) return device_status(e);
+    return device_status(bana::launch_merge_pieces(ws_out, ws_lse, prefix, plan.K, d->batch, d->num_q_heads,
+                                                   g0 * a.G, ng * a.G, out, lse, s));
+  }
   if (plan.nc == 1) {
     a.out = out;
     a.lse = lse;
@@ -268,7 +336,7 @@ bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, c
                                 float* out, float* lse_out, void* stream) {
   // Only the row count (batch x num_q_heads) and head_dim matter to the merge.
   if (d == nullptr || d->batch <= 0 || d->num_q_heads <= 0 || d->head_dim <= 0) return BANA_ERR_INVALID;
-  if (d->head_dim != kHeadDim) return BANA_ERR_UNSUPPORTED;
+  if (d->head_dim != kHeadDim || (int64_t)d->batch * d->num_q_heads > INT32_MAX) return BANA_ERR_UNSUPPORTED;
   if (!out_partials || !lses || !out || n_parts < 1) return BANA_ERR_INVALID;
   if (!aligned16(out_partials) || !aligned16(out)) return BANA_ERR_INVALID;
   return device_status(bana::launch_merge(out_partials, lses, n_parts, d->batch, d->num_q_heads, 0, d->num_q_heads, out,
@@ -329,7 +397,6 @@ bana_status bana_debug_gather_read(const bana_dims* d, const void* k_cache, cons
   if (!k_cache || !v_cache || !block_table || !kv_range_begin || !kv_range_end || !sink || n_parts < 1)
     return BANA_ERR_INVALID;
   if (!aligned16(k_cache) || !aligned16(v_cache)) return BANA_ERR_INVALID;
-  if ((int64_t)d->batch * d->num_kv_heads > INT32_MAX) return BANA_ERR_UNSUPPORTED;  // one workgroup per (b, g)
   return device_status(bana::launch_gather_read(k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts,
                                                 d->batch, d->num_kv_heads, d->max_blocks_per_seq, sink,
                                                 static_cast<hipStream_t>(stream)));

@@ -27,6 +27,18 @@ struct PartialArgs {
 // Partial attention: one workgroup of `waves` wavefronts per (chunk, sequence, kv head).
 hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stream);
 
+constexpr int kBalancedWaves = 8;       // wavefronts per workgroup of the balanced launch
+constexpr int kMaxBalancedBatch = 64;  // one sequence per lane of the in-kernel schedule
+
+// Balanced launch: K wavefronts per kv head, each over an equal interval of the call's virtual
+// blocks; a.out / a.lse are piece buffers [K + B][Hq][128] / [K + B][Hq]; prefix [B + 1]
+// receives the block-count prefix sums over sequences (for the merge).
+hipError_t launch_balanced_attn(const PartialArgs& a, int32_t* prefix, int K, hipStream_t stream);
+
+// Merge of the balanced launch's pieces into out / lse_out [B][Hq] rows of heads [h0, h0 + hn).
+hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, int64_t B,
+                               int Hq, int h0, int hn, float* out, float* lse_out, hipStream_t stream);
+
 // Log-sum-exp merge of n_parts partials over the rows (b, h) of B sequences x Hq heads restricted
 // to heads [h0, h0 + hn): partials are [n_parts][B][Hq][128] / [n_parts][B][Hq], outputs [B][Hq][128].
 hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn,

@@ -84,12 +84,19 @@ __global__ __launch_bounds__(256) void merge_few_kernel(const float* __restrict_
 constexpr int kUnroll = 4;  // partial rows in flight per lane
 
 // Any number of parts.  Group k (of KP) of a row takes parts k, k + KP, ...;
-// its q-th part is p = k + KP q.
-template <int KP>
+// its q-th part is p = k + KP q.  Part p of output row `row` is row
+// base + p * prow of the part buffers: base = row and prow = B x Hq for
+// partials [n_parts][B][Hq]; for the balanced launch's pieces, base is the
+// row's head in the sequence's first piece slot and prow = Hq (the slots of
+// a sequence's pieces are consecutive), and the part count comes from the
+// block-count prefix sums (pieces = intervals of S blocks that overlap the
+// sequence's blocks [prefix[b], prefix[b + 1])).
+template <int KP, bool PIECES>
 __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict__ outs,
                                                          const float* __restrict__ lses, int n_parts, int64_t B,
                                                          int Hq, int h0, int hn, float* __restrict__ out,
-                                                         float* __restrict__ lse_out) {
+                                                         float* __restrict__ lse_out,
+                                                         const int32_t* __restrict__ prefix, int K) {
   constexpr int R = 256 / (32 * KP);  // rows per workgroup
   __shared__ f32x4 sm_acc[KP > 1 ? R * KP * 32 : 1];
   __shared__ float sm_m[KP > 1 ? R * KP : 1];
@@ -99,13 +106,30 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
   const int k = (t >> 5) % KP;
   const int rl = t / (32 * KP);
   const int64_t r = (int64_t)blockIdx.x * R + rl;  // row among the B x hn merged rows
-  const int64_t rows = B * Hq;                      // row stride of one part
   const bool live = r < B * hn;
   const int64_t row = live ? (r / hn) * Hq + h0 + r % hn : 0;
-  const int nq = live && n_parts > k ? (n_parts - k + KP - 1) / KP : 0;
-  const int64_t lstride = (int64_t)KP * rows;                  // from the q-th part of the group to the next
-  const float* lrow = lses + (int64_t)k * rows + row;           // lse of the q-th part: lrow[q * lstride]
-  const float* orow = outs + ((int64_t)k * rows + row) * 128;  // its row: orow + q * lstride * 128
+  int64_t base = row;
+  int64_t prow = B * Hq;
+  int n = n_parts;
+  if (PIECES) {
+    n = 0;
+    prow = Hq;
+    if (live) {
+      const int64_t b = r / hn;
+      const int p0 = prefix[b], p1 = prefix[b + 1], U = prefix[B];
+      const int64_t S = U > K ? ((int64_t)U + K - 1) / K : 1;
+      if (p1 > p0) {  // slots clamped to [b, K + b): prefix sums from another call cannot reach outside
+        const int64_t first = min(max((int64_t)p0 / S, (int64_t)0), (int64_t)K - 1);
+        const int64_t last = min(max((int64_t)(p1 - 1) / S, first), (int64_t)K - 1);
+        n = (int)(last - first + 1);
+        base = (first + b) * Hq + h0 + r % hn;
+      }
+    }
+  }
+  const int nq = live && n > k ? (n - k + KP - 1) / KP : 0;
+  const int64_t lstride = (int64_t)KP * prow;                   // from the q-th part of the group to the next
+  const float* lrow = lses + (int64_t)k * prow + base;           // lse of the q-th part: lrow[q * lstride]
+  const float* orow = outs + ((int64_t)k * prow + base) * 128;  // its row: orow + q * lstride * 128
 
   // Group max: lane d4 reads parts q = d4, d4 + 32, ...
   float l0 = -INFINITY;
@@ -122,9 +146,9 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
       // Weight of part q0 + d4 on lane d4 (0 past the end and for empty parts).
       const float lq = q0 == 0 ? l0 : (q0 + d4 < nq ? lrow[(q0 + d4) * lstride] : -INFINITY);
       const float wq = lq == -INFINITY ? 0.f : expf(lq - m);
-      const int n = min(32, nq - q0);
+      const int nr = min(32, nq - q0);  // parts of this round
       int j = 0;
-      for (; j + kUnroll <= n; j += kUnroll) {
+      for (; j + kUnroll <= nr; j += kUnroll) {
         f32x4 o[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
@@ -136,7 +160,7 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
           if (w != 0.f) acc += w * o[u];
         }
       }
-      for (; j < n; ++j) {
+      for (; j < nr; ++j) {
         const f32x4 o = reinterpret_cast<const f32x4*>(orow + (q0 + j) * lstride * 128)[d4];
         const float w = __shfl(wq, j, 32);
         wsum += w;
@@ -180,14 +204,15 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
   if (lse_out != nullptr && d4 == 0) lse_out[row] = M + logf(wsum);
 }
 
-template <int KP>
+template <int KP, bool PIECES = false>
 hipError_t launch_many(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn,
-                       float* out, float* lse_out, hipStream_t stream) {
+                       float* out, float* lse_out, hipStream_t stream, const int32_t* prefix = nullptr,
+                       int K = 0) {
   constexpr int R = 256 / (32 * KP);
   const int64_t rows = B * hn;
   const unsigned grid = (unsigned)((rows + R - 1) / R);
-  hipLaunchKernelGGL(merge_many_kernel<KP>, dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, B, Hq, h0, hn,
-                     out, lse_out);
+  hipLaunchKernelGGL((merge_many_kernel<KP, PIECES>), dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, B, Hq,
+                     h0, hn, out, lse_out, prefix, K);
   return hipGetLastError();
 }
 
@@ -211,6 +236,14 @@ hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64
     if (n_parts >= 8) return launch_many<2>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
   }
   return launch_many<1>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
+}
+
+hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, int64_t B,
+                               int Hq, int h0, int hn, float* out, float* lse_out, hipStream_t stream) {
+  if (B * hn == 0) return hipSuccess;
+  // Few rows come with long sequences, hence many pieces per row: spread them over 8 thread groups.
+  if (B * Hq < 4096) return launch_many<8, true>(outs, lses, 0, B, Hq, h0, hn, out, lse_out, stream, prefix, K);
+  return launch_many<1, true>(outs, lses, 0, B, Hq, h0, hn, out, lse_out, stream, prefix, K);
 }
 
 }  // namespace bana

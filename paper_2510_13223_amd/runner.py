@@ -30,7 +30,7 @@ class DeviceWorkload:
     """Device-resident inputs and outputs of one workload, plus prepared call arguments."""
 
     def __init__(self, w, device="cuda", waves_hint: int = 0, chunks_hint: int = 0, use_workspace: bool = True,
-                 range_hints: bool = True, order_hints: bool = True):
+                 range_hints: bool = True, order_hints: bool = True, plan_hint: int = 0):
         self.w = w
         self.device = torch.device(device)
         self.q = _bf16(w.q, self.device)
@@ -62,7 +62,7 @@ class DeviceWorkload:
                                             max_range_tokens=int(lens.max()) if range_hints else 0,
                                             waves_hint=waves_hint, chunks_hint=chunks_hint,
                                             total_range_tokens=int(lens.sum()) if range_hints else 0,
-                                            seq_order=self._orders[-1]))
+                                            seq_order=self._orders[-1], plan_hint=plan_hint))
         # The fused call sees each sequence's ranges as one concatenated range.
         lens_all = (w.kv_end.astype(np.int64) - w.kv_begin).sum(axis=0)
         self._orders.append(order(lens_all))
@@ -70,14 +70,16 @@ class DeviceWorkload:
                                          max_range_tokens=int(lens_all.max()) if range_hints else 0,
                                          waves_hint=waves_hint, chunks_hint=chunks_hint,
                                          total_range_tokens=int(lens_all.sum()) if range_hints else 0,
-                                         seq_order=self._orders[-1])
+                                         seq_order=self._orders[-1], plan_hint=plan_hint)
         self.fused_out = torch.empty((B, Hq, bana.HEAD_DIM), dtype=torch.float32, device=self.device)
         self.fused_lse = torch.empty((B, Hq), dtype=torch.float32, device=self.device)
         ws = max(bana.bana_decode_attn_workspace_bytes(d) for d in self.dims + [self.fused_dims]) if use_workspace else 0
         self.workspace: Optional[torch.Tensor] = (
             torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device) if ws > 0 else None)
-        # Validate every argument once through the checked binding (this also runs the step once).
+        # Validate every argument once through the checked binding (this also runs the step once), and
+        # wait for it: calls on other streams must not overlap it, since they share the workspace.
         self.run_checked()
+        torch.cuda.synchronize(self.device)
         self._prepare_fast_args()
 
     def run_checked(self, stream=None) -> None:

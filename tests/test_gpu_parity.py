@@ -116,22 +116,57 @@ def test_launch_plans_agree(waves, chunks):
 def test_without_workspace_runs_unsplit():
     w = _workload("tiny", 2)
     _full_parity(w, use_workspace=False, range_hints=False)
+    _full_parity(w, use_workspace=False, plan_hint=2)  # the balanced launch needs workspace: runs unsplit
 
 
-def test_run_to_run_bit_determinism():
-    w = _workload("tiny", 0)
-    dw = DeviceWorkload(w)
-    a = dw.results()
+@pytest.mark.parametrize("seed,plan", [(0, 1), (1, 1), (0, 2), (1, 2), (2, 2)])
+def test_forced_launch_shapes(seed, plan):
+    """The chunked (1) and the balanced (2) launch on the tiny workload; balanced there has fewer
+    blocks than wavefronts (one block per wavefront, most wavefronts idle)."""
+    _full_parity(_workload("tiny", seed), plan_hint=plan)
+
+
+@pytest.mark.parametrize("name", ["long", "mixed"])
+def test_chunked_launch_on_uneven_workloads(name):
+    """long and mixed pick the balanced launch by themselves; the chunked one must still meet the bar."""
+    _full_parity(_workload(name), plan_hint=1)
+
+
+@pytest.mark.parametrize("B,every", [(64, 13), (300, 97)])
+def test_balanced_launch_with_runs_of_empty_sequences(B, every):
+    """Only every `every`-th sequence has tokens in partition 0 (runs of empty sequences between
+    pieces), one sequence is long, range ends are ragged.  With 64 sequences the balanced launch runs
+    (one sequence per lane of its schedule); with 300 the hint falls back to the chunked launch."""
+    rng = np.random.default_rng(B)
+    lens = rng.integers(1, 400, size=B)
+    lens[B // 2] = 5000
+    ranges = [[], []]
+    for b in range(B):
+        L = int(lens[b])
+        cut = int(rng.integers(1, L + 1)) if (b % every == 3 or b == B // 2) else 0
+        ranges[0].append((0, cut))
+        ranges[1].append((cut, L))
+    w = W.make_custom(21, B, 8, 2, lens, ranges, q_scale=1 / math.sqrt(128))
+    _full_parity(w, plan_hint=2)
+
+
+@pytest.mark.parametrize("name,plan", [("tiny", 0), ("tiny", 2), ("mixed", 0)])
+def test_run_to_run_bit_determinism(name, plan):
+    w = _workload(name, 0)
+    dw = DeviceWorkload(w, plan_hint=plan)
+    a = dw.results() + dw.fused_results()
     dw.step()
-    b = dw.results()
+    dw.fused(__import__("ctypes").c_void_p(torch.cuda.current_stream().cuda_stream))
+    b = dw.results() + dw.fused_results()
     for x, y in zip(a, b):
         assert np.array_equal(x, y, equal_nan=True)
 
 
-def test_physical_block_permutation_bit_identical():
+@pytest.mark.parametrize("plan", [0, 2])
+def test_physical_block_permutation_bit_identical(plan):
     w = _workload("tiny", 0)
-    a = DeviceWorkload(w).results()
-    b = DeviceWorkload(W.permute_physical(w, 3)).results()
+    a = DeviceWorkload(w, plan_hint=plan).results()
+    b = DeviceWorkload(W.permute_physical(w, 3), plan_hint=plan).results()
     for x, y in zip(a, b):
         assert np.array_equal(x, y, equal_nan=True)
 
@@ -167,12 +202,12 @@ def _aim_dominant(w, part, seed):
     return chosen
 
 
-@pytest.mark.parametrize("waves,chunks", [(0, 0), (1, 1), (8, 3)])
-def test_dominant_key_returns_value_row_exactly(waves, chunks):
+@pytest.mark.parametrize("waves,chunks,plan", [(0, 0, 0), (1, 1, 0), (8, 3, 0), (0, 0, 2)])
+def test_dominant_key_returns_value_row_exactly(waves, chunks, plan):
     w = W.make_config("tiny", 3)
     chosen = {part: _aim_dominant(w, part, 10 + part) for part in range(w.n_parts)}
-    _log(f"[dominant] waves={waves} chunks={chunks}")
-    op, lp, _, _ = DeviceWorkload(w, waves_hint=waves, chunks_hint=chunks).results()
+    _log(f"[dominant] waves={waves} chunks={chunks} plan={plan}")
+    op, lp, _, _ = DeviceWorkload(w, waves_hint=waves, chunks_hint=chunks, plan_hint=plan).results()
     for part, picks in chosen.items():
         for (b, g), t in picks.items():
             blk = w.block_table[b, t // 16]
@@ -181,7 +216,8 @@ def test_dominant_key_returns_value_row_exactly(waves, chunks):
 
 
 def test_zero_keys_pin_coverage_counts():
-    for name, kw in (("tiny", {}), ("tiny", dict(waves_hint=4, chunks_hint=5)), ("mixed", {})):
+    for name, kw in (("tiny", {}), ("tiny", dict(waves_hint=4, chunks_hint=5)), ("tiny", dict(plan_hint=2)),
+                     ("mixed", {})):
         w = W.make_config(name, 0)
         finite = np.isfinite(W.bf16_bits_to_f32(w.k_cache))
         w.k_cache[finite] = 0

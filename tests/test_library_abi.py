@@ -52,7 +52,7 @@ def _dims(**kw):
     base.update(kw)
     d = bana.make_dims(base["batch"], base["num_q_heads"], base["num_kv_heads"], base["max_blocks_per_seq"],
                        base["num_blocks"])
-    for k in ("head_dim", "block_size", "reserved", "waves_hint", "chunks_hint", "max_range_tokens"):
+    for k in ("head_dim", "block_size", "plan_hint", "waves_hint", "chunks_hint", "max_range_tokens"):
         if k in kw:
             setattr(d, k, kw[k])
     return d
@@ -68,7 +68,7 @@ def _partial(lib, d, ptrs=None, ws=None, ws_bytes=0):
 
 @pytest.mark.parametrize("kw,expect", [
     (dict(batch=0), -1), (dict(num_q_heads=-8), -1), (dict(num_kv_heads=3), -1), (dict(num_blocks=0), -1),
-    (dict(max_blocks_per_seq=0), -1), (dict(reserved=1), -1), (dict(waves_hint=3), -1), (dict(chunks_hint=-1), -1),
+    (dict(max_blocks_per_seq=0), -1), (dict(plan_hint=3), -1), (dict(plan_hint=-1), -1), (dict(waves_hint=3), -1), (dict(chunks_hint=-1), -1),
     (dict(max_range_tokens=-5), -1),
     (dict(head_dim=64), -2), (dict(block_size=32), -2), (dict(num_q_heads=34, num_kv_heads=2), -2),
 ])
@@ -204,3 +204,11 @@ def test_gather_read_rejects_bad_arguments(lib):
     assert lib.bana_debug_gather_read(ctypes.byref(d), *args, 1, None, None) == -1
     assert lib.bana_debug_gather_read(ctypes.byref(d), ctypes.c_void_p(0x100008), *args[1:], 1, FAKE, None) == -1
     assert lib.bana_debug_gather_read(ctypes.byref(_dims(head_dim=64)), *args, 1, FAKE, None) == -2
+
+
+def test_sizes_beyond_32_bit_indices_are_unsupported(lib):
+    big = _dims(batch=1 << 20, num_q_heads=4096, num_kv_heads=4096, max_blocks_per_seq=1)
+    assert _partial(lib, big) == -2
+    assert lib.bana_merge_partials(ctypes.byref(big), FAKE, FAKE, 2, FAKE, None, None) == -2
+    assert _partial(lib, _dims(batch=1 << 16, max_blocks_per_seq=1 << 16)) == -2
+    assert _partial(lib, _dims(batch=1, max_blocks_per_seq=1 << 28)) == -2
