@@ -133,6 +133,17 @@ def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape=None):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
 
 
+def _check_dims(dims: bana_dims, q: torch.Tensor, k_cache: torch.Tensor, block_table: torch.Tensor) -> None:
+    """Caller-built dims must describe the tensors passed with them (the kernels index by the dims)."""
+    B, Hq, D = q.shape
+    nb, Hkv = k_cache.shape[0], k_cache.shape[1]
+    got = (dims.batch, dims.num_q_heads, dims.num_kv_heads, dims.head_dim, dims.max_blocks_per_seq, dims.num_blocks)
+    want = (B, Hq, Hkv, D, block_table.shape[1], nb)
+    if got != want:
+        raise ValueError(f"dims (batch, Hq, Hkv, head_dim, max_blocks_per_seq, num_blocks) = {got} "
+                         f"do not match the tensors {want}")
+
+
 def dims_for(q: torch.Tensor, k_cache: torch.Tensor, block_table: torch.Tensor, max_range_tokens: int = 0,
              waves_hint: int = 0, chunks_hint: int = 0, total_range_tokens: int = 0) -> bana_dims:
     B, Hq, D = q.shape
@@ -169,6 +180,7 @@ def bana_decode_attn_partial(q, k_cache, v_cache, block_table, seq_lens, kv_rang
         ws_bytes = workspace.numel() * workspace.element_size()
     if dims is None:
         dims = dims_for(q, k_cache, block_table, max_range_tokens)
+    _check_dims(dims, q, k_cache, block_table)
     st = lib().bana_decode_attn_partial(
         ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens),
         _ptr(kv_range_begin), _ptr(kv_range_end), _ptr(out_partial), _ptr(lse), _ptr(workspace), ws_bytes,
@@ -210,6 +222,7 @@ def bana_decode_attn_fused(q, k_cache, v_cache, block_table, seq_lens, kv_range_
         ws_bytes = workspace.numel() * workspace.element_size()
     if dims is None:
         dims = dims_for(q, k_cache, block_table)
+    _check_dims(dims, q, k_cache, block_table)
     st = lib().bana_decode_attn_fused(
         ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens),
         _ptr(kv_range_begin), _ptr(kv_range_end), n, _ptr(out), _ptr(lse_out), _ptr(workspace), ws_bytes,
@@ -233,6 +246,7 @@ def bana_decode_attn_heads(q, k_cache, v_cache, block_table, seq_lens, kv_range_
         ws_bytes = workspace.numel() * workspace.element_size()
     if dims is None:
         dims = dims_for(q, k_cache, block_table)
+    _check_dims(dims, q, k_cache, block_table)
     st = lib().bana_decode_attn_heads(
         ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens),
         _ptr(kv_range_begin), _ptr(kv_range_end), int(kv_head_begin), int(kv_head_end), _ptr(out), _ptr(lse),

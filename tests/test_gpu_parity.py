@@ -358,6 +358,14 @@ def test_non_default_stream_and_binding_checks():
     with pytest.raises(TypeError):
         bana.bana_decode_attn_partial(dw.q.float(), dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens,
                                       dw.kv_begin[0], dw.kv_end[0], dw.out_partials[0], dw.lses[0])
+    # caller-built dims that do not describe the tensors are refused before any launch
+    bad = bana.make_dims(w.batch, w.num_q_heads, w.num_kv_heads, w.max_blocks_per_seq, w.num_blocks * 4)
+    with pytest.raises(ValueError):
+        bana.bana_decode_attn_partial(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin[0],
+                                      dw.kv_end[0], dw.out_partials[0], dw.lses[0], dims=bad)
+    with pytest.raises(ValueError):
+        bana.bana_decode_attn_fused(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin,
+                                    dw.kv_end, dw.fused_out, dw.fused_lse, dims=bad)
 
 
 @pytest.mark.parametrize("name,part", [("tiny", 0), ("tiny", 1), ("llama3_8b", 1), ("mixed", 1)])
