@@ -615,3 +615,17 @@ def test_gather_read_covers_exactly_the_attention_tiles(seed):
                                     torch.from_numpy(end).cuda(), sink)
         got = sink.cpu().numpy().view(np.uint32)
         np.testing.assert_array_equal(got, _gather_xor_ref(w, begin, end))
+
+
+def test_plain_c_caller_through_the_abi():
+    """A C program (tests/c/abi_roundtrip.c: hipMalloc'd buffers, its own stream, no Python or torch)
+    runs the per-partition calls, the merge and the fused call and checks them against the oracle."""
+    import os
+    import subprocess
+
+    exe = os.path.join(os.path.dirname(os.path.abspath(__file__)), "c", "abi_roundtrip")
+    assert os.path.exists(exe), "build it first: python __graft_entry__.py (or python tests/c/build.py)"
+    _log("[c-abi] running tests/c/abi_roundtrip")
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    _log(r.stdout.strip())
+    assert r.returncode == 0, r.stdout + r.stderr

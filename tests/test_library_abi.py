@@ -245,3 +245,23 @@ def test_plan_choice_between_chunked_and_balanced(lib):
     assert ws(8, 32, 8, 77000, 8 * 25000, plan_hint=1) != _balanced_bytes(8, 32, 8)
     # too few blocks for one round of wavefronts: no balanced launch without the hint
     assert ws(4, 8, 2, 1000, 4 * 300) != _balanced_bytes(4, 8, 2)
+
+
+def _c_build_module():
+    import importlib.util
+
+    spec = importlib.util.spec_from_file_location("abi_roundtrip_build", os.path.join(ROOT, "tests", "c", "build.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_plain_c_caller_builds_against_the_header(lib):
+    """The C ABI is usable from C: a program including only include/bana.h (and HIP's runtime API)
+    compiles with -Wall and links libbana.so; tests/test_gpu_parity.py runs it on the GPU."""
+    import oracle
+
+    if not os.path.exists(oracle.LIB_PATH):
+        oracle.build()
+    path = _c_build_module().build()
+    assert os.access(path, os.X_OK)
