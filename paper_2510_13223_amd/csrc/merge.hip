@@ -152,7 +152,7 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
         f32x4 o[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
-          o[u] = reinterpret_cast<const f32x4*>(orow + (q0 + j + u) * lstride * 128)[d4];
+          o[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(orow + (q0 + j + u) * lstride * 128) + d4);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
           const float w = __shfl(wq, j + u, 32);
@@ -161,7 +161,7 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
         }
       }
       for (; j < nr; ++j) {
-        const f32x4 o = reinterpret_cast<const f32x4*>(orow + (q0 + j) * lstride * 128)[d4];
+        const f32x4 o = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(orow + (q0 + j) * lstride * 128) + d4);
         const float w = __shfl(wq, j, 32);
         wsum += w;
         if (w != 0.f) acc += w * o;
