@@ -206,6 +206,16 @@ class LayerPipeline:
                  self.host_store_v[i].view(torch.int16).numpy().view(np.uint16)) for i in range(self.L)]
 
 
+def t_kv_ms(s_kv_bytes: float, tokens: int, hit_rate: float, link_gbps: float) -> float:
+    """Per-layer KV transfer time of the store (Sec. 4.2): S_kv x L x r over the link bandwidth, in ms."""
+    return s_kv_bytes * tokens * hit_rate * 8 / (link_gbps * 1e9) * 1e3
+
+
+def t_f_layer_ms(t_f_ms: float, hit_rate: float, layers: int) -> float:
+    """Per-layer forward time of the same example (Sec. 4.2): T_F x r / N, in ms."""
+    return t_f_ms * hit_rate / layers
+
+
 def measure(workload: str = "llama3_8b", layers: int = 8, fetch_tokens: int = 500, store_tokens: int = 500,
             reps: int = 5) -> dict:
     """Per-layer times of the serial and the pipelined schedules, and the measured T_KV.
@@ -249,7 +259,7 @@ def measure(workload: str = "llama3_8b", layers: int = 8, fetch_tokens: int = 50
         "stage_ms_fetch_attend_store": [round(float(x), 5) for x in stage],
         "t_kv_measured_ms": round(float(stage[0]), 5),
         "h2d_gbs": round(fetch_bytes / (float(stage[0]) / 1e3) / 1e9, 2),
-        "t_kv_formula_ms_at_200gbps": round(s_kv * fetch_tokens / (200e9 / 8) * 1e3, 5),
+        "t_kv_formula_ms_at_200gbps": round(t_kv_ms(s_kv, fetch_tokens, 1.0, 200.0), 5),
     }
 
 

@@ -359,3 +359,18 @@ def test_migrated_partition_attends_identically(seed, part):
     untouched = np.setdiff1d(np.arange(m.num_blocks), used)
     assert untouched.size > 0 and np.all(dk[untouched] == W.SENTINEL) and np.all(dv[untouched] == W.SENTINEL)
     assert used.size == int(np.sum(m.blk_end - m.blk_begin))
+
+
+def test_paper_worked_example_pipeline_times():
+    """Sec. 4.2 worked example of the layer pipeline: T_F,layer ~ 4.22 ms and T_KV ~ 0.082 ms (printed to
+    the digits shown), and the transfer the pipeline measures is the same formula at its own sizes."""
+    from paper_2510_13223_amd import pipeline
+
+    g = json.load(open(os.path.join(GOLDEN, "pipeline_worked_example.json")))
+    t_f = pipeline.t_f_layer_ms(g["t_f_ms"], g["hit_rate"], g["layers"])
+    t_kv = pipeline.t_kv_ms(g["s_kv_bytes_per_token_per_layer"], g["tokens"], g["hit_rate"], g["link_gbps"])
+    assert round(t_f, 2) == g["t_f_layer_ms_printed"]
+    assert round(t_kv, 3) == g["t_kv_ms_printed"]
+    assert t_kv < t_f  # the transfer hides under the layer's compute
+    # 500 tokens at 4096 B per token over 200 Gbps: the figure the pipeline measurement reports beside its T_KV
+    assert abs(pipeline.t_kv_ms(4096, 500, 1.0, 200) - 0.08192) < 1e-12
