@@ -298,7 +298,7 @@ def test_fused_overlapping_empty_and_many_ranges():
         ranges.append(row)
     w = W.make_custom(5, len(lens), 8, 2, lens, ranges, q_scale=1 / math.sqrt(128))
     _log("[fused] 64 overlapping ranges")
-    for kw in ({}, dict(waves_hint=8, chunks_hint=3), dict(waves_hint=1, chunks_hint=1)):
+    for kw in ({}, dict(waves_hint=8, chunks_hint=3), dict(waves_hint=1, chunks_hint=1), dict(plan_hint=2)):
         _fused_vs_oracle(w, **kw)
 
 
@@ -313,8 +313,13 @@ def test_fused_dominant_key_and_all_empty():
         blk = w.block_table[b, t // 16]
         assert np.array_equal(fo[b, g * w.group], W.bf16_bits_to_f32(w.v_cache[blk, g, :, t % 16]))
     empty = dataclasses.replace(w, kv_begin=w.kv_end.copy())
-    fo, fl = DeviceWorkload(empty).fused_results()
-    assert np.all(fo == 0.0) and np.all(np.isneginf(fl))
+    for plan in (0, 2):  # chunked, balanced (no blocks at all: every wavefront idle, every row empty)
+        dw = DeviceWorkload(empty, plan_hint=plan)
+        op, lp, out, lse_out = dw.results()
+        fo, fl = dw.fused_results()
+        assert np.all(fo == 0.0) and np.all(np.isneginf(fl))
+        assert np.all(out == 0.0) and np.all(np.isneginf(lse_out))
+        assert np.all(op == 0.0) and np.all(np.isneginf(lp))
 
 
 # (parts, batch, heads): the few-part kernel, and the many-part kernel with 1, 2, 4 and 8 thread
