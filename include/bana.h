@@ -33,7 +33,10 @@
  *    0 <= kv_range_begin[b] <= kv_range_end[b] <= seq_lens[b], and every
  *    block-table entry for a block that overlaps [begin, end) names a block
  *    of the pool.  Entries outside the covered blocks are never read.
- *    bana_validate_ranges checks them on the device when wanted.
+ *    bana_validate_ranges checks them on the device when wanted.  The
+ *    optional dispatch order (bana_dims.seq_order) must be a permutation of
+ *    0..batch-1 for every row to be written; out-of-range entries are
+ *    clamped, never followed.
  *
  * Layouts (bf16 = IEEE binary16-brain, stored as 2 bytes)
  * --------------------------------------------------------

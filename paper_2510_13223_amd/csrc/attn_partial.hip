@@ -320,7 +320,8 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   int wg = blockIdx.x;
   const int g = a.g0 + wg % a.ng;
   wg /= a.ng;
-  const int b = a.seq_order != nullptr ? table_lookup(a.seq_order, 0, 0, wg % a.B) : wg % a.B;
+  // The dispatch order is a hint: an entry outside [0, B) is clamped, never followed.
+  const int b = a.seq_order != nullptr ? min(max(table_lookup(a.seq_order, 0, 0, wg % a.B), 0), a.B - 1) : wg % a.B;
   const int c = wg / a.B;
   const int G = a.G;
   const int hq0 = g * G;
