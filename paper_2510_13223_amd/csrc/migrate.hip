@@ -9,8 +9,8 @@
 // contiguous run (Hkv x 4 KiB for K, the same for V), so a block is two
 // contiguous copies.  A grid row per sequence whose workgroups stride over the
 // sequence's migrated blocks (the row width only sets parallelism); each
-// thread moves 16 bytes per step with non-temporal loads and stores (the data
-// is touched once).  HBM-bound: reads and writes Hkv x 8 KiB per block.
+// thread moves 16 bytes per step, non-temporal loads (the source is read
+// once), plain stores.  HBM-bound: reads and writes Hkv x 8 KiB per block.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -59,9 +59,9 @@ __global__ __launch_bounds__(kThreads) void migrate_kernel(const u32x4* __restri
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         const int64_t i = i0 + (int64_t)u * kThreads;
-        if (i < n16) {
-          __builtin_nontemporal_store(kx[u], dk + i);
-          __builtin_nontemporal_store(vx[u], dv + i);
+        if (i < n16) {  // plain stores: measured ~4 % faster than non-temporal ones for this scatter
+          dk[i] = kx[u];
+          dv[i] = vx[u];
         }
       }
     }
