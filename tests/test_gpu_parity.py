@@ -628,8 +628,16 @@ def test_plain_c_caller_through_the_abi():
     import os
     import subprocess
 
-    exe = os.path.join(os.path.dirname(os.path.abspath(__file__)), "c", "abi_roundtrip")
-    assert os.path.exists(exe), "build it first: python __graft_entry__.py (or python tests/c/build.py)"
+    here = os.path.dirname(os.path.abspath(__file__))
+    exe = os.path.join(here, "c", "abi_roundtrip")
+    if not os.path.exists(exe):  # normally built by __graft_entry__.build(); gcc takes a second
+        import importlib.util
+
+        oracle._load()  # builds liboracle.so if it is missing
+        spec = importlib.util.spec_from_file_location("abi_roundtrip_build", os.path.join(here, "c", "build.py"))
+        mod = importlib.util.module_from_spec(spec)
+        spec.loader.exec_module(mod)
+        mod.build()
     _log("[c-abi] running tests/c/abi_roundtrip")
     r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     _log(r.stdout.strip())
