@@ -12,10 +12,15 @@ block 16, seq_len 4096, last 30 % of each sequence's blocks migrated ->
 
 Prints ONE JSON line.  ``value`` is the KV-read bandwidth of the whole step
 (K+V bytes of all covered tokens / step time); ``tokens_per_s`` is decode
-tokens (sequences) per second for the layer.  ``roofline`` reports the
-partial-attention kernel against the 8 TB/s HBM peak, timed with HIP events
-on the stream it runs on.  ``cpu_baseline`` times the fp64 CPU oracle on the
-same workload on this host.
+tokens (sequences) per second for the layer.  ``cold_cache`` times the step
+alone with a cache scrub in between; ``gather_read_ceiling`` reads the same
+tiles with no arithmetic (the access pattern's practical ceiling).
+``roofline`` reports the partial-attention kernel against the 8 TB/s HBM
+peak, timed with HIP events on the stream it runs on, with the HBM bytes of
+the committed counter summary when it matches the kernel sources.
+``migration`` times the KV-block copy of the migrated partition.
+``cpu_baseline`` times the fp64 CPU oracle on the same workload on this host
+(all cores, plus a single-core sample).
 """
 
 from __future__ import annotations
