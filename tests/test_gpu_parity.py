@@ -642,3 +642,26 @@ def test_plain_c_caller_through_the_abi():
     r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     _log(r.stdout.strip())
     assert r.returncode == 0, r.stdout + r.stderr
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_shapes_every_launch_shape(case):
+    """Seeded random small workloads (batch, GQA group, lengths, 1-5 ranges per sequence with empty,
+    one-token and ragged ranges) through the automatic, chunked and balanced plans, per-partition and
+    fused, against the oracle."""
+    rng = np.random.default_rng(1000 + case)
+    B = int(rng.integers(1, 13))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    Hq = Hkv * int(rng.choice([1, 2, 4, 8, 16]))
+    n_parts = int(rng.integers(1, 6))
+    lens = [int(x) for x in rng.integers(1, 2500, size=B)]
+    ranges = [[] for _ in range(n_parts)]
+    for L in lens:
+        cuts = np.sort(rng.integers(0, L + 1, size=n_parts - 1)).tolist()
+        edges = [0] + cuts + [L]
+        for p in range(n_parts):
+            ranges[p].append((edges[p], edges[p + 1]))
+    w = W.make_custom(50 + case, B, Hq, Hkv, lens, ranges, q_scale=1 / math.sqrt(128))
+    _log(f"[random {case}] B={B} Hq={Hq} Hkv={Hkv} parts={n_parts}")
+    for plan in (0, 1, 2):
+        _full_parity(w, plan_hint=plan)
