@@ -324,6 +324,11 @@ def main():
     achieved = mean_bytes / mean_dur_s / 1e9
     partial_kv_gbs = float(np.sum([a[1] for a in alg])) / (float(dur_ms.sum(axis=1).mean()) / 1e3) / 1e9
 
+    # One kernel per partial call when no partition's plan needs workspace; otherwise the call is the
+    # attention kernel plus its chunk (or piece) merge, and the events time both.
+    single = all(bana.bana_decode_attn_workspace_bytes(d) == 0 for d in dw.dims)
+    roofline_kernel = ("partial_attn_kernel" if single else
+                       "bana_decode_attn_partial call (attention kernel + chunk or piece merge)")
     line = {
         "metric": METRIC,
         "value": round(kv_bytes / t_step / 1e9, 2),
@@ -364,6 +369,8 @@ def main():
             "entry_point": "bana_debug_gather_read",
             "what": "the step's K/V tiles read through the block table with the attention kernel's load shapes, "
                     "no arithmetic",
+            # one workgroup of 8 wavefronts per (sequence, kv head): a ceiling only when those fill one round
+            "comparable": w.batch * w.num_kv_heads >= 512,
             "us": round(gather_s * 1e6, 2),
             "value": round(kv_bytes / gather_s / 1e9, 2),
             "unit": "GB/s",
@@ -380,7 +387,7 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "partial_attn_kernel",
+            "kernel": roofline_kernel,
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
