@@ -224,9 +224,9 @@ struct Online {
 struct Segments {
   int t0, t1, jfirst, nblk, vend;
 
-  __device__ __forceinline__ void load(const PartialArgs& a, int b, int lane) {
+  __device__ __forceinline__ void load(const PartialArgs& a, int b, int lane, int n_parts) {
     t0 = t1 = jfirst = nblk = 0;
-    if (lane < a.n_parts) {
+    if (lane < n_parts) {
       t0 = a.begin[(int64_t)lane * a.B + b];
       t1 = a.end[(int64_t)lane * a.B + b];
       if (t1 > t0) {
@@ -235,6 +235,7 @@ struct Segments {
       }
     }
     vend = nblk;
+    if (n_parts == 1) return;  // one range: lane 0 holds it, nothing to sum
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const int y = __shfl_up(vend, off);
@@ -272,14 +273,14 @@ __device__ __forceinline__ void seek(const Segments& sg, Seg& c, int v, int n_pa
 // so about one block (8 KiB) per wave stays in flight through the softmax and
 // MFMA work.  Table entries are read two blocks ahead with scalar loads.
 template <int STEP>
-__device__ __forceinline__ void walk_blocks(Online& st, const bf16x8 (&qop)[4], const Segments& sg,
+__device__ __forceinline__ void walk_blocks(Online& st, const bf16x8 (&qop)[4], const Segments& sg, int n_parts,
                                             const PartialArgs& a, int b, int g, int col, int quad, int jr, int jb1) {
   if (jr >= jb1) return;
   const int vlast = jb1 - 1;
   Seg cm = seg_at(sg, 0);  // segment of the block being computed
   Seg ct = cm;             // segment of the block whose table entry is read
   auto table_at = [&](int v) {
-    seek(sg, ct, v, a.n_parts);
+    seek(sg, ct, v, n_parts);
     return table_lookup(a.table, a.max_blocks, b, ct.jfirst + (v - ct.vstart));
   };
   const int32_t blk_first = table_at(jr);
@@ -299,19 +300,22 @@ __device__ __forceinline__ void walk_blocks(Online& st, const bf16x8 (&qop)[4], 
     const int64_t tile_next = kv_tile(blk_next, g, a.Hkv);
     const f32x4 s = block_scores(qop, kr);
     load_k(kr, a.k, tile_next, col, quad);
-    seek(sg, cm, jr, a.n_parts);
+    seek(sg, cm, jr, n_parts);
     st.update(s, vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1, quad);
     load_v(vr, a.v, tile_next, col, quad);
     jr += STEP;
     blk_next = blk_after;
   }
-  seek(sg, cm, jr, a.n_parts);
+  seek(sg, cm, jr, n_parts);
   st.update(block_scores(qop, kr), vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1, quad);
 }
 
-template <int W>
+// MULTI: the call passes several ranges per sequence (the fused entry point); a
+// single range (one partition) compiles the segment handling away.
+template <int W, bool MULTI>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) void partial_attn_kernel(PartialArgs a) {
   extern __shared__ float smem[];
+  const int n_parts = MULTI ? a.n_parts : 1;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int col = lane & 15;  // query head in group (score/output column); token row for K; dim for V
@@ -327,8 +331,8 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   const int hq0 = g * G;
 
   Segments sg;
-  sg.load(a, b, lane);
-  const int nblk = sg.total(a.n_parts);
+  sg.load(a, b, lane, n_parts);
+  const int nblk = sg.total(n_parts);
   int per = (nblk + a.nc - 1) / a.nc;
   if (per < a.cmin) per = a.cmin;
   const int nch = nblk > 0 ? (nblk + per - 1) / per : 0;
@@ -353,7 +357,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   load_q(qop, a.q, (int64_t)b * a.Hq + hq0, col, quad, G);
   Online st;
   st.init();
-  walk_blocks<W>(st, qop, sg, a, b, g, col, quad, jb0 + wave, jb1);
+  walk_blocks<W>(st, qop, sg, n_parts, a, b, g, col, quad, jb0 + wave, jb1);
 
   if (W == 1) {
     st.emit(out_dst, lse_dst, col, quad, G);
@@ -443,7 +447,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     const int b = __builtin_popcountll(__ballot(lane < a.B && incl <= pos));  // sequence holding block pos
     const int pb = b > 0 ? __builtin_amdgcn_readlane(incl, b - 1) : 0;
     Segments sg;
-    sg.load(a, b, lane);
+    sg.load(a, b, lane, a.n_parts);
     const int nb = sg.total(a.n_parts);
     const int v0 = pos - pb;
     const int v1 = min(u1 - pb, nb);
@@ -452,7 +456,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     load_q(qop, a.q, (int64_t)b * a.Hq + hq0, col, quad, G);
     Online st;
     st.init();
-    walk_blocks<1>(st, qop, sg, a, b, g, col, quad, v0, v1);
+    walk_blocks<1>(st, qop, sg, a.n_parts, a, b, g, col, quad, v0, v1);
     const int64_t row0 = (int64_t)(k + b) * a.Hq + hq0;
     st.emit(a.out + row0 * kHeadDim, a.lse + row0, col, quad, G);
     pos = pb + v1;
@@ -464,11 +468,24 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
 hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stream) {
   const unsigned nwg = (unsigned)a.nc * (unsigned)a.B * (unsigned)a.ng;
   const size_t smem = waves > 1 ? sizeof(float) * (size_t)(32 * waves + waves * a.G * kRowPad) : 0;
+  const bool multi = a.n_parts > 1;
   switch (waves) {
-    case 1: hipLaunchKernelGGL(partial_attn_kernel<1>, dim3(nwg), dim3(64), smem, stream, a); break;
-    case 2: hipLaunchKernelGGL(partial_attn_kernel<2>, dim3(nwg), dim3(128), smem, stream, a); break;
-    case 4: hipLaunchKernelGGL(partial_attn_kernel<4>, dim3(nwg), dim3(256), smem, stream, a); break;
-    case 8: hipLaunchKernelGGL(partial_attn_kernel<8>, dim3(nwg), dim3(512), smem, stream, a); break;
+    case 1:
+      if (multi) hipLaunchKernelGGL((partial_attn_kernel<1, true>), dim3(nwg), dim3(64), smem, stream, a);
+      else hipLaunchKernelGGL((partial_attn_kernel<1, false>), dim3(nwg), dim3(64), smem, stream, a);
+      break;
+    case 2:
+      if (multi) hipLaunchKernelGGL((partial_attn_kernel<2, true>), dim3(nwg), dim3(128), smem, stream, a);
+      else hipLaunchKernelGGL((partial_attn_kernel<2, false>), dim3(nwg), dim3(128), smem, stream, a);
+      break;
+    case 4:
+      if (multi) hipLaunchKernelGGL((partial_attn_kernel<4, true>), dim3(nwg), dim3(256), smem, stream, a);
+      else hipLaunchKernelGGL((partial_attn_kernel<4, false>), dim3(nwg), dim3(256), smem, stream, a);
+      break;
+    case 8:
+      if (multi) hipLaunchKernelGGL((partial_attn_kernel<8, true>), dim3(nwg), dim3(512), smem, stream, a);
+      else hipLaunchKernelGGL((partial_attn_kernel<8, false>), dim3(nwg), dim3(512), smem, stream, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
