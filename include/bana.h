@@ -132,7 +132,7 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
 
 /*
  * Head-split partition: the literal reading of Sec. 4.1(2), where the KV
- * cache is split "along the attention head dimension" -- KV_1 keeps some kv
+ * cache is split along the attention heads -- KV_1 keeps some kv
  * heads on the hot device, KV_2 the others on the cold device.  Computes, for
  * the kv heads [kv_head_begin, kv_head_end) only, exactly what
  * bana_decode_attn_partial computes for them over the same range, bit for bit
