@@ -14,7 +14,9 @@ Prints ONE JSON line.  ``value`` is the KV-read bandwidth of the whole step
 (K+V bytes of all covered tokens / step time); ``tokens_per_s`` is decode
 tokens (sequences) per second for the layer.  ``cold_cache`` times the step
 alone with a cache scrub in between; ``gather_read_ceiling`` reads the same
-tiles with no arithmetic (the access pattern's practical ceiling).
+tiles with no arithmetic (the access pattern's practical ceiling);
+``stream_read_ceiling`` reads both block pools front to back (HBM's
+streaming-read ceiling on this GPU).
 ``roofline`` reports the partial-attention kernel against the 8 TB/s HBM
 peak, timed with HIP events on the stream it runs on, with the HBM bytes of
 the committed counter summary when it matches the kernel sources.
@@ -260,6 +262,25 @@ def main():
     gather_s = (time.perf_counter() - wall0) / args.steps
     print(f"[bench] gather-read ceiling: {gather_s * 1e6:.1f} us", file=sys.stderr, flush=True)
 
+    # Streaming ceiling of HBM reads: both pools read front to back (bana_debug_stream_read,
+    # 2048 workgroups of 256 threads = 32 resident wavefronts per CU).
+    stream_sink = torch.empty(2048, dtype=torch.int32, device=dev)
+    pool_bytes = 2 * dw.k_cache.numel() * dw.k_cache.element_size()
+
+    def stream_read():
+        bana.bana_debug_stream_read(dw.k_cache, stream_sink, stream=stream)
+        bana.bana_debug_stream_read(dw.v_cache, stream_sink, stream=stream)
+
+    for _ in range(args.warmup):
+        stream_read()
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for _ in range(args.steps):
+        stream_read()
+    torch.cuda.synchronize()
+    stream_s = (time.perf_counter() - wall0) / args.steps
+    print(f"[bench] stream-read ceiling: {stream_s * 1e6:.1f} us for {pool_bytes} B", file=sys.stderr, flush=True)
+
     # Timed region 2: the same K steps with HIP events recorded on the stream the kernel runs on:
     # (a) one pair around each step's partial-attention launches (back to back, the merge after
     # the second event), which gives the kernel's mean launch duration for the roofline; (b) one
@@ -385,6 +406,17 @@ def main():
             "value": round(kv_bytes / gather_s / 1e9, 2),
             "unit": "GB/s",
             "frac_of_hbm_peak": round(kv_bytes / gather_s / 1e9 / HBM_PEAK_GBS, 4),
+        },
+        "stream_read_ceiling": {
+            "entry_point": "bana_debug_stream_read",
+            "what": "both block pools read front to back (two launches), 16-byte non-temporal loads, "
+                    "32 wavefronts per CU, no arithmetic",
+            "comparable": pool_bytes >= (256 << 20),
+            "bytes": pool_bytes,
+            "us": round(stream_s * 1e6, 2),
+            "value": round(pool_bytes / stream_s / 1e9, 2),
+            "unit": "GB/s",
+            "frac_of_hbm_peak": round(pool_bytes / stream_s / 1e9 / HBM_PEAK_GBS, 4),
         },
         "migration": {
             "entry_point": "bana_migrate_kv_blocks",

@@ -25,8 +25,9 @@
  *    num_q_heads % num_kv_heads != 0, n_parts < 1 or a misaligned pointer;
  *    BANA_ERR_UNSUPPORTED for head_dim != 128, block_size != 16, a GQA
  *    group (num_q_heads / num_kv_heads) above 16, or sizes whose indices
- *    leave 32 bits (batch * max_blocks_per_seq, max_blocks_per_seq * 16 or
- *    batch * num_q_heads above 2^31 - 1).
+ *    leave 32 bits (batch * max_blocks_per_seq or max_blocks_per_seq * 16
+ *    above 2^31 - 1, or batch * num_q_heads of 2^26 or more: a launch counts
+ *    its threads in 32 bits).
  *  - A failed launch returns BANA_ERR_DEVICE; bana_last_error() then holds
  *    the HIP error text (per calling thread).
  *  - Device-resident values are preconditions and are not checked per call:
@@ -92,7 +93,8 @@ typedef struct {
   int32_t chunks_hint;        /* chunks a range may be split into (needs workspace) */
   int32_t plan_hint;          /* 0 = choose; 1 = chunked launch; 2 = balanced launch
                                  (equal block intervals per wavefront across
-                                 sequences; needs workspace and batch <= 64,
+                                 sequences; needs workspace, batch <= 64 and
+                                 batch * 64 * max_blocks_per_seq <= 2^31 - 1,
                                  otherwise the chunked launch runs) */
   int64_t total_range_tokens; /* sum over sequences of kv_range_end - kv_range_begin */
   /* Optional device array [batch]: the order in which sequences are
@@ -170,7 +172,8 @@ size_t bana_decode_attn_workspace_bytes(const bana_dims* d);
  * dims->max_range_tokens / total_range_tokens, when given, refer to the sum
  * over a sequence's ranges.  Per-partition partials are not produced (use
  * bana_decode_attn_partial for those).  Errors as for the partial call;
- * n_parts > 64 gives BANA_ERR_UNSUPPORTED.
+ * n_parts > 64 or n_parts * max_blocks_per_seq above 2^31 - 1 gives
+ * BANA_ERR_UNSUPPORTED.
  */
 bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
                                    const int32_t* block_table, const int32_t* seq_lens,
@@ -285,6 +288,20 @@ bana_status bana_debug_kv_rows(const bana_dims* d, const int32_t* block_table, c
 bana_status bana_debug_gather_read(const bana_dims* d, const void* k_cache, const void* v_cache,
                                    const int32_t* block_table, const int32_t* kv_range_begin,
                                    const int32_t* kv_range_end, int32_t n_parts, uint32_t* sink, void* stream);
+
+/*
+ * Measurement hook: a plain front-to-back read of `bytes` bytes at src
+ * (device memory, 16-byte aligned, bytes a multiple of 16) by n_groups
+ * workgroups of 256 threads, each thread loading 16 bytes per step with a
+ * stride of n_groups * 256 * 16 bytes (the streaming-read ceiling of HBM, for
+ * comparison with the tile gather above; 8 workgroups per compute unit keep
+ * 32 wavefronts resident on each).  The words are XOR-folded so the loads
+ * cannot be dropped: the XOR of sink[0..n_groups) equals the XOR of all
+ * 32-bit words of the buffer.  sink: uint32 [n_groups] (device).
+ * BANA_ERR_INVALID for a NULL pointer, misalignment, or n_groups outside
+ * [1, 65536].
+ */
+bana_status bana_debug_stream_read(const void* src, size_t bytes, int32_t n_groups, uint32_t* sink, void* stream);
 
 #ifdef __cplusplus
 }

@@ -91,6 +91,8 @@ def lib() -> ctypes.CDLL:
     L.bana_debug_kv_rows.restype = ctypes.c_int
     L.bana_debug_gather_read.argtypes = [D, P, P, P, P, P, ctypes.c_int32, P, P]
     L.bana_debug_gather_read.restype = ctypes.c_int
+    L.bana_debug_stream_read.argtypes = [P, ctypes.c_size_t, ctypes.c_int32, P, P]
+    L.bana_debug_stream_read.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -352,3 +354,38 @@ def bana_debug_gather_read(k_cache, v_cache, block_table, kv_range_begin, kv_ran
                                       _ptr(kv_range_begin), _ptr(kv_range_end), n, _ptr(sink), _stream(stream))
     if st != BANA_OK:
         raise BanaError(st, "bana_debug_gather_read")
+
+
+def bana_debug_stream_read(buf: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
+    """Front-to-back read of the bytes of ``buf`` (contiguous device tensor, size a multiple of 16) by
+    ``sink.numel()`` workgroups; ``sink`` uint32 as int32 [n_groups].
+
+    See ``bana_debug_stream_read`` in include/bana.h (the XOR of the sink words is the XOR of the
+    buffer's 32-bit words).
+    """
+    if not isinstance(buf, torch.Tensor) or buf.device.type != "cuda" or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    _need(sink, "sink", torch.int32)
+    nbytes = buf.numel() * buf.element_size()
+    st = lib().bana_debug_stream_read(_ptr(buf), nbytes, sink.numel(), _ptr(sink), _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_debug_stream_read")
+
+
+def bana_copy_async(dst: torch.Tensor, src: torch.Tensor, stream=None) -> None:
+    """Stream-ordered copy of all bytes of ``src`` into ``dst`` by the library's copy kernel.
+
+    Both contiguous, the same number of bytes (a multiple of 16), on the device or in pinned host
+    memory; see ``bana_copy_async`` in include/bana.h.
+    """
+    for t, name in ((dst, "dst"), (src, "src")):
+        if not isinstance(t, torch.Tensor) or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous tensor")
+        if t.device.type != "cuda" and not t.is_pinned():
+            raise ValueError(f"{name} must be device or pinned host memory")
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("dst and src differ in size")
+    st = lib().bana_copy_async(_ptr(dst), _ptr(src), nbytes, _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_copy_async")

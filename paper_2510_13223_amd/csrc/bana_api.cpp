@@ -26,6 +26,8 @@ constexpr int kMinBlocksPerWave = 8;    // below this a wavefront spends more ti
 constexpr int kMaxBlocksPerWave = 64;   // longest run of blocks one wavefront should walk (no hints)
 constexpr int kMaxChunks = 256;
 constexpr int kMaxFusedParts = 64;  // one range per lane of the segment table
+constexpr int64_t kMaxRows = int64_t{1} << 26;  // batch x num_q_heads: 64 threads per row stay below 2^32
+constexpr int64_t kMaxLaunchItems = UINT32_MAX;  // work-items of one launch (grid x workgroup size)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -42,11 +44,12 @@ bana_status check_dims(const bana_dims* d) {
     return BANA_ERR_INVALID;
   if (d->head_dim != kHeadDim || d->block_size != kBlockSize) return BANA_ERR_UNSUPPORTED;
   if (d->num_q_heads / d->num_kv_heads > kMaxGroup) return BANA_ERR_UNSUPPORTED;
-  // Index arithmetic of the kernels: table rows, token indices, workgroup
-  // indices (one per sequence and kv head at least) and output rows are 32-bit.
+  // Index arithmetic of the kernels: table rows and token indices are
+  // 32-bit, and a launch counts its work-items in 32 bits (one wavefront per
+  // (sequence, kv head) at least; 32 threads per output row in the merge).
   if ((int64_t)d->batch * d->max_blocks_per_seq > INT32_MAX ||
       (int64_t)d->max_blocks_per_seq * kBlockSize > INT32_MAX ||
-      (int64_t)d->batch * d->num_q_heads > INT32_MAX)
+      (int64_t)d->batch * d->num_q_heads >= kMaxRows)
     return BANA_ERR_UNSUPPORTED;
   return BANA_OK;
 }
@@ -99,7 +102,10 @@ Plan make_plan(const bana_dims* d) {
   Plan p;
   p.balanced = false;
   p.K = std::max(1, kTargetWaves / (bana::kBalancedWaves * d->num_kv_heads)) * bana::kBalancedWaves;
-  if (d->batch <= bana::kMaxBalancedBatch && d->waves_hint == 0 && d->chunks_hint == 0 && d->plan_hint != 1) {
+  // The balanced schedule counts the blocks of all ranges of all sequences in 32 bits.
+  const bool fits32 = (int64_t)d->batch * kMaxFusedParts * d->max_blocks_per_seq <= INT32_MAX;
+  if (d->batch <= bana::kMaxBalancedBatch && fits32 && d->waves_hint == 0 && d->chunks_hint == 0 &&
+      d->plan_hint != 1) {
     const int64_t call_blocks = hinted ? d->total_range_tokens / kBlockSize + d->batch : 0;
     const bool few_pairs = pairs < kTargetWaves / bana::kBalancedWaves;
     const bool very_uneven = hinted && 2 * bound > 3 * mean_blocks;  // longest range > 1.5 x mean
@@ -121,6 +127,7 @@ Plan make_plan(const bana_dims* d) {
   // The cross-wave combine keeps W * G rows of 132 floats in LDS; stay within 64 KiB per workgroup.
   const int G = d->num_q_heads / d->num_kv_heads;
   while (p.waves > 1 && sizeof(float) * (size_t)(32 * p.waves + p.waves * G * (kHeadDim + 4)) > 65536) p.waves /= 2;
+  while (p.waves > 1 && pairs * 64 * p.waves > kMaxLaunchItems) p.waves /= 2;
   if (d->chunks_hint > 0) {
     p.nc = d->chunks_hint;
     p.cmin = 1;
@@ -147,7 +154,7 @@ Plan make_plan(const bana_dims* d) {
     p.cmin = p.waves * 16;
   }
   p.nc = std::max(1, std::min(p.nc, kMaxChunks));
-  if ((int64_t)p.nc * pairs > INT32_MAX) p.nc = 1;
+  if ((int64_t)p.nc * pairs * 64 * p.waves > kMaxLaunchItems) p.nc = 1;
   return p;
 }
 
@@ -306,6 +313,8 @@ bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void
       !lse_out || n_parts < 1)
     return BANA_ERR_INVALID;
   if (n_parts > kMaxFusedParts) return BANA_ERR_UNSUPPORTED;
+  // A sequence's blocks over all its ranges are counted in 32 bits.
+  if ((int64_t)n_parts * d->max_blocks_per_seq > INT32_MAX) return BANA_ERR_UNSUPPORTED;
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out) ||
       (workspace != nullptr && !aligned16(workspace)))
     return BANA_ERR_INVALID;
@@ -336,7 +345,7 @@ bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, c
                                 float* out, float* lse_out, void* stream) {
   // Only the row count (batch x num_q_heads) and head_dim matter to the merge.
   if (d == nullptr || d->batch <= 0 || d->num_q_heads <= 0 || d->head_dim <= 0) return BANA_ERR_INVALID;
-  if (d->head_dim != kHeadDim || (int64_t)d->batch * d->num_q_heads > INT32_MAX) return BANA_ERR_UNSUPPORTED;
+  if (d->head_dim != kHeadDim || (int64_t)d->batch * d->num_q_heads >= kMaxRows) return BANA_ERR_UNSUPPORTED;
   if (!out_partials || !lses || !out || n_parts < 1) return BANA_ERR_INVALID;
   if (!aligned16(out_partials) || !aligned16(out)) return BANA_ERR_INVALID;
   return device_status(bana::launch_merge(out_partials, lses, n_parts, d->batch, d->num_q_heads, 0, d->num_q_heads, out,
@@ -400,6 +409,12 @@ bana_status bana_debug_gather_read(const bana_dims* d, const void* k_cache, cons
   return device_status(bana::launch_gather_read(k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts,
                                                 d->batch, d->num_kv_heads, d->max_blocks_per_seq, sink,
                                                 static_cast<hipStream_t>(stream)));
+}
+
+bana_status bana_debug_stream_read(const void* src, size_t bytes, int32_t n_groups, uint32_t* sink, void* stream) {
+  if (!src || !sink || bytes % 16 != 0 || !aligned16(src) || n_groups < 1 || n_groups > 65536)
+    return BANA_ERR_INVALID;
+  return device_status(bana::launch_stream_read(src, bytes, n_groups, sink, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -37,6 +37,7 @@ __global__ __launch_bounds__(256) void debug_rows_kernel(const int32_t* __restri
 hipError_t launch_debug_rows(const int32_t* table, const int32_t* begin, const int32_t* end, int B, int Hkv,
                              int max_blocks, int64_t* rows, hipStream_t stream) {
   const int64_t n = (int64_t)B * Hkv * max_blocks * kBlockSize;
+  if ((n + 255) / 256 > (int64_t)UINT32_MAX / 256) return hipErrorInvalidValue;  // grid x limit
   const unsigned grid = (unsigned)((n + 255) / 256);
   hipLaunchKernelGGL(debug_rows_kernel, dim3(grid), dim3(256), 0, stream, table, begin, end, B, Hkv, max_blocks,
                      rows);

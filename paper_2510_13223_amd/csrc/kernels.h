@@ -66,6 +66,10 @@ hipError_t launch_gather_read(const void* k, const void* v, const int32_t* table
                               const int32_t* end, int n_parts, int B, int Hkv, int max_blocks, uint32_t* sink,
                               hipStream_t stream);
 
+// Sequential read of `bytes` (a multiple of 16) by n_groups workgroups of 256 threads;
+// sink[w] = XOR of the 32-bit words workgroup w read.
+hipError_t launch_stream_read(const void* src, size_t bytes, int n_groups, uint32_t* sink, hipStream_t stream);
+
 // Address export for the tests (rows of the K pool visited per logical token).
 hipError_t launch_debug_rows(const int32_t* table, const int32_t* begin, const int32_t* end, int B, int Hkv,
                              int max_blocks, int64_t* rows, hipStream_t stream);

@@ -102,7 +102,10 @@ hipError_t launch_migrate(const void* src_k, const void* src_v, const int32_t* s
                           const int32_t* dst_table, const int32_t* blk_begin, const int32_t* blk_end, int B,
                           int max_blocks, int max_migrated_blocks, int Hkv, hipStream_t stream) {
   if (max_migrated_blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(migrate_kernel, dim3((unsigned)max_migrated_blocks, (unsigned)B), dim3(kThreads), 0, stream,
+  // The row width only sets parallelism (workgroups stride over the blocks); keep the row's
+  // work-items well inside 32 bits.
+  const unsigned row = (unsigned)std::min(max_migrated_blocks, 1 << 16);
+  hipLaunchKernelGGL(migrate_kernel, dim3(row, (unsigned)B), dim3(kThreads), 0, stream,
                      static_cast<const u32x4*>(src_k), static_cast<const u32x4*>(src_v), src_table,
                      static_cast<u32x4*>(dst_k), static_cast<u32x4*>(dst_v), dst_table, blk_begin, blk_end,
                      max_blocks, Hkv);

@@ -26,27 +26,28 @@ __global__ __launch_bounds__(256) void validate_kernel(const int32_t* __restrict
                                                        const int32_t* __restrict__ begin,
                                                        const int32_t* __restrict__ end, int B, int max_blocks,
                                                        int64_t num_blocks, int32_t* result) {
-  const int b = blockIdx.x;
   const int p = blockIdx.y;
-  const int t0 = begin[(int64_t)p * B + b];
-  const int t1 = end[(int64_t)p * B + b];
-  const int L = seq_lens[b];
-  int code = 0;
-  if (L < 0 || (int64_t)L > (int64_t)max_blocks * kBlockSize) code = 3;
-  else if (t0 < 0 || t0 > t1) code = 1;
-  else if (t1 > L) code = 2;
-  if (code != 0) {
-    if (threadIdx.x == 0) atomicMax(result, code);
-    return;
+  for (int b = blockIdx.x; b < B; b += gridDim.x) {
+    const int t0 = begin[(int64_t)p * B + b];
+    const int t1 = end[(int64_t)p * B + b];
+    const int L = seq_lens[b];
+    int code = 0;
+    if (L < 0 || (int64_t)L > (int64_t)max_blocks * kBlockSize) code = 3;
+    else if (t0 < 0 || t0 > t1) code = 1;
+    else if (t1 > L) code = 2;
+    if (code != 0) {
+      if (threadIdx.x == 0) atomicMax(result, code);
+      continue;
+    }
+    if (t1 == t0) continue;
+    const int j0 = t0 / kBlockSize, j1 = (t1 - 1) / kBlockSize;
+    bool bad = false;
+    for (int j = j0 + (int)threadIdx.x; j <= j1; j += (int)blockDim.x) {
+      const int32_t blk = table[(int64_t)b * max_blocks + j];
+      bad |= blk < 0 || (int64_t)blk >= num_blocks;
+    }
+    if (bad) atomicMax(result, 4);
   }
-  if (t1 == t0) return;
-  const int j0 = t0 / kBlockSize, j1 = (t1 - 1) / kBlockSize;
-  bool bad = false;
-  for (int j = j0 + (int)threadIdx.x; j <= j1; j += (int)blockDim.x) {
-    const int32_t blk = table[(int64_t)b * max_blocks + j];
-    bad |= blk < 0 || (int64_t)blk >= num_blocks;
-  }
-  if (bad) atomicMax(result, 4);
 }
 
 }  // namespace
@@ -57,7 +58,9 @@ hipError_t launch_validate(const int32_t* table, const int32_t* seq_lens, const 
   hipLaunchKernelGGL(zero_kernel, dim3(1), dim3(1), 0, stream, result);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(validate_kernel, dim3((unsigned)B, (unsigned)n_parts), dim3(256), 0, stream, table, seq_lens,
+  // Workgroups stride over the sequences; the row width only sets parallelism.
+  const unsigned row = (unsigned)(B < (1 << 16) ? B : (1 << 16));
+  hipLaunchKernelGGL(validate_kernel, dim3(row, (unsigned)n_parts), dim3(256), 0, stream, table, seq_lens,
                      begin, end, B, max_blocks, num_blocks, result);
   return hipGetLastError();
 }

@@ -622,6 +622,85 @@ def test_gather_read_covers_exactly_the_attention_tiles(seed):
         np.testing.assert_array_equal(got, _gather_xor_ref(w, begin, end))
 
 
+def test_hooks_stride_past_their_grid():
+    """The validation and gather kernels stride over sequences / (sequence, kv head) pairs when there are
+    more than their grids hold (65,536 sequences; 2^20 pairs): every sequence is still checked and every
+    pair read."""
+    rng = np.random.default_rng(7)
+    B, Hkv, nb = 140_000, 8, 512  # 1.12 M pairs
+    _log(f"[hooks] B={B} Hkv={Hkv} pool={nb}")
+    k = rng.integers(0, 1 << 16, size=(nb, Hkv, 16, 16, 8), dtype=np.uint16)
+    v = rng.integers(0, 1 << 16, size=(nb, Hkv, 128, 16), dtype=np.uint16)
+    table = rng.integers(0, nb, size=(B, 1), dtype=np.int32)
+    end = rng.integers(0, 17, size=(1, B), dtype=np.int32)  # 0..16 tokens of the one block; 0 = empty
+    begin = np.zeros((1, B), dtype=np.int32)
+    dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a).view(dt)).cuda()
+    sink = torch.zeros((B, Hkv), dtype=torch.int32, device="cuda")
+    bana.bana_debug_gather_read(dev(k, np.int16).view(torch.bfloat16), dev(v, np.int16).view(torch.bfloat16),
+                                dev(table, np.int32), dev(begin, np.int32), dev(end, np.int32), sink)
+    tile_x = (np.bitwise_xor.reduce(k.reshape(nb, Hkv, -1).view(np.uint32), axis=2)
+              ^ np.bitwise_xor.reduce(v.reshape(nb, Hkv, -1).view(np.uint32), axis=2))
+    ref = np.where((end[0] > 0)[:, None], tile_x[table[:, 0]], np.uint32(0))
+    np.testing.assert_array_equal(sink.cpu().numpy().view(np.uint32), ref)
+
+    res = torch.empty(1, dtype=torch.int32, device="cuda")
+    Bv = 70_000
+    lens = np.full(Bv, 16, dtype=np.int32)
+    tb = table[:Bv].copy()
+
+    def check(tbl, e):
+        bana.bana_validate_ranges(dev(tbl, np.int32), dev(lens, np.int32), dev(np.zeros(Bv, np.int32), np.int32),
+                                  dev(e, np.int32), nb, res)
+        torch.cuda.synchronize()
+        return int(res.item())
+
+    e = np.full(Bv, 16, dtype=np.int32)
+    assert check(tb, e) == 0
+    e2 = e.copy(); e2[Bv - 1] = 17  # the last sequence, beyond the grid's first pass
+    assert check(tb, e2) == 2
+    tb2 = tb.copy(); tb2[Bv - 2, 0] = nb
+    assert check(tb2, e) == 4
+
+
+@pytest.mark.parametrize("nbytes,groups", [(16, 1), (4096 + 16, 7), ((1 << 20) + 48, 2048), (64 << 20, 2048)])
+def test_stream_read_folds_every_word(nbytes, groups):
+    """The streaming-read hook reads every 16-byte unit once: sink[w] is the XOR of the units
+    w*256 + t + i*groups*256, so their XOR is the XOR of the whole buffer."""
+    _log(f"[stream-read] bytes={nbytes} groups={groups}")
+    rng = np.random.default_rng(nbytes)
+    words = rng.integers(0, 1 << 32, size=nbytes // 4, dtype=np.uint32)
+    buf = torch.from_numpy(words.view(np.int32)).cuda()
+    sink = torch.full((groups,), -1, dtype=torch.int32, device="cuda")
+    bana.bana_debug_stream_read(buf, sink)
+    got = sink.cpu().numpy().view(np.uint32)
+    unit_x = np.bitwise_xor.reduce(words.reshape(-1, 4), axis=1)
+    grp = (np.arange(unit_x.size) // 256) % groups
+    ref = np.zeros(groups, dtype=np.uint32)
+    np.bitwise_xor.at(ref, grp, unit_x)
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_copy_binding_device_and_pinned_host():
+    """bana_copy_async through its checked binding: device to device, pinned host to device and back,
+    bit for bit, at a size that leaves a ragged last workgroup."""
+    n = (3 << 20) + 16
+    rng = np.random.default_rng(3)
+    host = torch.from_numpy(rng.integers(0, 256, size=n, dtype=np.uint8)).pin_memory()
+    dev_a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dev_b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    back = torch.empty(n, dtype=torch.uint8).pin_memory()
+    s = torch.cuda.Stream()
+    bana.bana_copy_async(dev_a, host, stream=s)
+    bana.bana_copy_async(dev_b, dev_a, stream=s)
+    bana.bana_copy_async(back, dev_b, stream=s)
+    s.synchronize()
+    assert torch.equal(back, host)
+    with pytest.raises(ValueError):
+        bana.bana_copy_async(dev_a[:16], dev_b[:32])
+    with pytest.raises(ValueError):
+        bana.bana_copy_async(dev_a, torch.zeros(n, dtype=torch.uint8))  # pageable host memory
+
+
 def test_plain_c_caller_through_the_abi():
     """A C program (tests/c/abi_roundtrip.c: hipMalloc'd buffers, its own stream, no Python or torch)
     runs the per-partition calls, the merge and the fused call and checks them against the oracle."""

@@ -206,12 +206,31 @@ def test_gather_read_rejects_bad_arguments(lib):
     assert lib.bana_debug_gather_read(ctypes.byref(_dims(head_dim=64)), *args, 1, FAKE, None) == -2
 
 
+def test_stream_read_rejects_bad_arguments(lib):
+    assert lib.bana_debug_stream_read(None, 4096, 8, FAKE, None) == -1
+    assert lib.bana_debug_stream_read(FAKE, 4096, 8, None, None) == -1
+    assert lib.bana_debug_stream_read(FAKE, 4100, 8, FAKE, None) == -1
+    assert lib.bana_debug_stream_read(ctypes.c_void_p(0x100008), 4096, 8, FAKE, None) == -1
+    assert lib.bana_debug_stream_read(FAKE, 4096, 0, FAKE, None) == -1
+    assert lib.bana_debug_stream_read(FAKE, 4096, 65537, FAKE, None) == -1
+
+
 def test_sizes_beyond_32_bit_indices_are_unsupported(lib):
     big = _dims(batch=1 << 20, num_q_heads=4096, num_kv_heads=4096, max_blocks_per_seq=1)
     assert _partial(lib, big) == -2
     assert lib.bana_merge_partials(ctypes.byref(big), FAKE, FAKE, 2, FAKE, None, None) == -2
     assert _partial(lib, _dims(batch=1 << 16, max_blocks_per_seq=1 << 16)) == -2
     assert _partial(lib, _dims(batch=1, max_blocks_per_seq=1 << 28)) == -2
+    # a launch counts work-items in 32 bits: batch x num_q_heads stays below 2^26
+    at = _dims(batch=1 << 20, num_q_heads=64, num_kv_heads=8)
+    below = _dims(batch=(1 << 20) - 1, num_q_heads=64, num_kv_heads=8)
+    assert _partial(lib, at) == -2
+    assert lib.bana_merge_partials(ctypes.byref(at), FAKE, FAKE, 2, FAKE, None, None) == -2
+    # just below the limit the dims pass, and n_parts = 0 is the error reported
+    assert lib.bana_merge_partials(ctypes.byref(below), FAKE, FAKE, 0, FAKE, None, None) == -1
+    # fused: a sequence's blocks over all its ranges are counted in 32 bits
+    wide = _dims(batch=1, max_blocks_per_seq=1 << 26)
+    assert lib.bana_decode_attn_fused(ctypes.byref(wide), *[FAKE] * 7, 64, FAKE, FAKE, None, 0, None) == -2
 
 
 def _balanced_bytes(B, Hq, Hkv):
@@ -245,6 +264,13 @@ def test_plan_choice_between_chunked_and_balanced(lib):
     assert ws(8, 32, 8, 77000, 8 * 25000, plan_hint=1) != _balanced_bytes(8, 32, 8)
     # too few blocks for one round of wavefronts: no balanced launch without the hint
     assert ws(4, 8, 2, 1000, 4 * 300) != _balanced_bytes(4, 8, 2)
+    # a table too wide for the balanced schedule's 32-bit block counts (batch x 64 ranges x width):
+    # the hint falls back to the chunked plan
+    wide = bana.make_dims(4, 8, 2, 1 << 23, 100000, max_range_tokens=1000, total_range_tokens=4 * 900, plan_hint=2)
+    assert lib.bana_decode_attn_workspace_bytes(ctypes.byref(wide)) != _balanced_bytes(4, 8, 2)
+    narrow = bana.make_dims(4, 8, 2, (1 << 23) - 1, 100000, max_range_tokens=1000, total_range_tokens=4 * 900,
+                            plan_hint=2)
+    assert lib.bana_decode_attn_workspace_bytes(ctypes.byref(narrow)) == _balanced_bytes(4, 8, 2)
 
 
 def _c_build_module():
