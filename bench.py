@@ -20,7 +20,9 @@ streaming-read ceiling on this GPU).
 ``roofline`` reports the partial-attention kernel against the 8 TB/s HBM
 peak, timed with HIP events on the stream it runs on, with the HBM bytes of
 the committed counter summary when it matches the kernel sources.
-``migration`` times the KV-block copy of the migrated partition.
+``migration`` times the KV-block copy of the migrated partition;
+``head_split`` times the head-split form of the method (each half of the kv
+heads over whole sequences, one ``bana_decode_attn_heads`` call each).
 ``cpu_baseline`` times the fp64 CPU oracle on the same workload on this host
 (all cores, plus a single-core sample).
 """
@@ -344,6 +346,43 @@ def main():
     del d_k, d_v
     print(f"[bench] migration: {mig_ms * 1e3:.1f} us for {mig_bytes / 1e6:.1f} MB", file=sys.stderr, flush=True)
 
+    # Timed region 5: the head split (the cache split along kv heads instead of tokens): each half of
+    # the kv heads over whole sequences, one bana_decode_attn_heads call each, timed by events.
+    hs_begin = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+    hs_end = dw.seq_lens
+    lens_all = w.seq_lens.astype(np.int64)
+    hs_dims = bana.make_dims(w.batch, w.num_q_heads, w.num_kv_heads, w.max_blocks_per_seq, w.num_blocks,
+                             max_range_tokens=int(lens_all.max()), total_range_tokens=int(lens_all.sum()))
+    hs_out = torch.empty((w.batch, w.num_q_heads, 128), dtype=torch.float32, device=dev)
+    hs_lse = torch.empty((w.batch, w.num_q_heads), dtype=torch.float32, device=dev)
+    half = w.num_kv_heads // 2
+    hs_ranges = [(0, half), (half, w.num_kv_heads)] if half > 0 else [(0, w.num_kv_heads)]
+    hs_ws = []
+    for g0, g1 in hs_ranges:
+        nbytes = bana.bana_decode_attn_workspace_bytes(bana.head_range_dims(hs_dims, g0, g1))
+        hs_ws.append(torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev))
+
+    def head_call(i):
+        g0, g1 = hs_ranges[i]
+        bana.bana_decode_attn_heads(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, hs_begin, hs_end,
+                                    g0, g1, hs_out, hs_lse, workspace=hs_ws[i], stream=stream, dims=hs_dims)
+
+    for _ in range(args.warmup):
+        for i in range(len(hs_ranges)):
+            head_call(i)
+    torch.cuda.synchronize()
+    hs_ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in hs_ranges]
+             for _ in range(args.steps)]
+    for row in hs_ev:
+        for i, (a, b) in enumerate(row):
+            a.record(stream)
+            head_call(i)
+            b.record(stream)
+    torch.cuda.synchronize()
+    hs_us = [float(np.mean([row[i][0].elapsed_time(row[i][1]) for row in hs_ev])) * 1e3 for i in range(len(hs_ranges))]
+    hs_bytes = [int(lens_all.sum()) * (g1 - g0) * 128 * 2 * 2 for g0, g1 in hs_ranges]
+    print(f"[bench] head split: {[round(x, 1) for x in hs_us]} us", file=sys.stderr, flush=True)
+
     kv_bytes = w.kv_bytes()
     t_step = ms_per_step / 1e3
     # Partial-attention kernel: algorithmic bytes over its own launch durations.
@@ -417,6 +456,17 @@ def main():
             "value": round(pool_bytes / stream_s / 1e9, 2),
             "unit": "GB/s",
             "frac_of_hbm_peak": round(pool_bytes / stream_s / 1e9 / HBM_PEAK_GBS, 4),
+        },
+        "head_split": {
+            "entry_point": "bana_decode_attn_heads",
+            "what": "the cache split along kv heads: each range of kv heads over whole sequences, one call each "
+                    "(what each device of a head split computes), HIP events around each call",
+            "kv_heads": [list(r) for r in hs_ranges],
+            "us_per_call": [round(x, 2) for x in hs_us],
+            "kv_bytes_per_call": hs_bytes,
+            "value": round(sum(hs_bytes) / (sum(hs_us) * 1e-6) / 1e9, 2),
+            "unit": "GB/s",
+            "frac_of_hbm_peak": round(sum(hs_bytes) / (sum(hs_us) * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         },
         "migration": {
             "entry_point": "bana_migrate_kv_blocks",

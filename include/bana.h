@@ -137,14 +137,21 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
  * cache is split along the attention heads -- KV_1 keeps some kv
  * heads on the hot device, KV_2 the others on the cold device.  Computes, for
  * the kv heads [kv_head_begin, kv_head_end) only, exactly what
- * bana_decode_attn_partial computes for them over the same range, bit for bit
- * (the launch plan is taken from the full dims), and writes only the rows of
- * their query heads (h with h / G in the kv-head range) of out / lse; other
- * rows are left untouched.  With head partitions the "merge" is the
- * concatenation of rows: calls over complementary kv-head ranges give the
- * full result.  An empty kv-head range does nothing.  Other arguments and
- * errors as for bana_decode_attn_partial; a kv-head range outside
- * [0, num_kv_heads] gives BANA_ERR_INVALID.
+ * bana_decode_attn_partial computes on the sub-problem made of those heads
+ * alone, bit for bit: q, the pools, out and lse holding only those heads
+ * (and their G query heads each), with dims whose num_kv_heads is
+ * kv_head_end - kv_head_begin and num_q_heads G times that.  That is what the
+ * device holding those heads computes after they migrate there, so the launch
+ * is planned for that many heads and fills the GPU by itself.  Only the rows
+ * of the range's query heads (h with h / G in the kv-head range) of out / lse
+ * are written; other rows are left untouched.  With head partitions the
+ * "merge" is the concatenation of rows: calls over complementary kv-head
+ * ranges give the full result (up to float rounding order, as the full call
+ * may plan its launch differently).  An empty kv-head range does nothing.
+ * workspace: as for bana_decode_attn_partial, sized by
+ * bana_decode_attn_workspace_bytes of the sub-problem's dims.  Other
+ * arguments and errors as for bana_decode_attn_partial; a kv-head range
+ * outside [0, num_kv_heads] gives BANA_ERR_INVALID.
  */
 bana_status bana_decode_attn_heads(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
                                    const int32_t* block_table, const int32_t* seq_lens,
@@ -152,9 +159,10 @@ bana_status bana_decode_attn_heads(const bana_dims* d, const void* q, const void
                                    int32_t kv_head_begin, int32_t kv_head_end, float* out, float* lse,
                                    void* workspace, size_t workspace_bytes, void* stream);
 
-/* Bytes of workspace bana_decode_attn_partial / bana_decode_attn_fused /
- * bana_decode_attn_heads can use for these dims (0 when they would not split
- * ranges); 0 for invalid dims. */
+/* Bytes of workspace bana_decode_attn_partial / bana_decode_attn_fused can
+ * use for these dims (0 when they would not split ranges); 0 for invalid
+ * dims.  For bana_decode_attn_heads, pass the sub-problem's dims (its kv
+ * heads only). */
 size_t bana_decode_attn_workspace_bytes(const bana_dims* d);
 
 /*

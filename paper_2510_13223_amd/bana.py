@@ -158,6 +158,16 @@ def bana_decode_attn_workspace_bytes(dims: bana_dims) -> int:
     return int(lib().bana_decode_attn_workspace_bytes(ctypes.byref(dims)))
 
 
+def head_range_dims(dims: bana_dims, kv_head_begin: int, kv_head_end: int) -> bana_dims:
+    """Dims of the sub-problem of kv heads [kv_head_begin, kv_head_end): what bana_decode_attn_heads
+    plans for, and what sizes its workspace."""
+    G = dims.num_q_heads // dims.num_kv_heads
+    sub = bana_dims.from_buffer_copy(dims)
+    sub.num_kv_heads = kv_head_end - kv_head_begin
+    sub.num_q_heads = G * (kv_head_end - kv_head_begin)
+    return sub
+
+
 def bana_decode_attn_partial(q, k_cache, v_cache, block_table, seq_lens, kv_range_begin, kv_range_end,
                              out_partial, lse, workspace: Optional[torch.Tensor] = None, stream=None,
                              dims: Optional[bana_dims] = None, max_range_tokens: int = 0) -> None:
@@ -236,7 +246,10 @@ def bana_decode_attn_fused(q, k_cache, v_cache, block_table, seq_lens, kv_range_
 def bana_decode_attn_heads(q, k_cache, v_cache, block_table, seq_lens, kv_range_begin, kv_range_end,
                            kv_head_begin: int, kv_head_end: int, out, lse, workspace: Optional[torch.Tensor] = None,
                            stream=None, dims: Optional[bana_dims] = None) -> None:
-    """Head-split partition: the kv heads [kv_head_begin, kv_head_end) only; see include/bana.h."""
+    """Head-split partition: the kv heads [kv_head_begin, kv_head_end) only; see include/bana.h.
+
+    The workspace is sized by ``bana_decode_attn_workspace_bytes(head_range_dims(dims, begin, end))``.
+    """
     B, Hq, D = _check_attn_inputs(q, k_cache, v_cache, block_table, seq_lens)
     _need(kv_range_begin, "kv_range_begin", torch.int32, (B,))
     _need(kv_range_end, "kv_range_end", torch.int32, (B,))

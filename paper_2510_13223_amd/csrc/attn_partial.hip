@@ -338,7 +338,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   const int nch = nblk > 0 ? (nblk + per - 1) / per : 0;
 
   // Destination of this workgroup's result.
-  const int64_t row0 = ((int64_t)(a.nc == 1 ? 0 : c) * a.B + b) * a.Hq + hq0;
+  const int64_t row0 = ((int64_t)(a.nc == 1 ? 0 : c) * a.B + b) * a.out_hq + hq0 - a.out_h0;
   float* __restrict__ out_dst = a.out + row0 * kHeadDim;
   float* __restrict__ lse_dst = a.lse + row0;
 
@@ -402,7 +402,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
 // Balanced launch (batch <= 64): wavefront k of kv head g walks the blocks
 // [k S, (k + 1) S) (clipped to U) of the call's virtual block list and leaves
 // one partial per sequence piece in slot k + b of the piece buffers
-// ([slot][Hq][128] and [slot][Hq]).  Every wavefront computes the schedule
+// ([slot][out_hq][128] and [slot][out_hq]).  Every wavefront computes the schedule
 // itself, one sequence per lane: block counts N_b, their prefix sums by lane
 // shuffles, U and S; the sequence holding block pos is the number of
 // sequences whose blocks end at or before pos.  The first wavefront of the
@@ -457,7 +457,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     Online st;
     st.init();
     walk_blocks<1>(st, qop, sg, a.n_parts, a, b, g, col, quad, v0, v1);
-    const int64_t row0 = (int64_t)(k + b) * a.Hq + hq0;
+    const int64_t row0 = (int64_t)(k + b) * a.out_hq + hq0 - a.out_h0;
     st.emit(a.out + row0 * kHeadDim, a.lse + row0, col, quad, G);
     pos = pb + v1;
   }

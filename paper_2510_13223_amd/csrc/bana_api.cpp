@@ -215,21 +215,28 @@ size_t bana_decode_attn_workspace_bytes(const bana_dims* d) {
 
 namespace {
 
-// Shared by the per-partition and the fused entry points: n_parts ranges per
-// sequence ([n_parts][B] begin / end), result (merged over the ranges) into
-// out / lse.  Chunked plans leave chunk partials in the workspace and merge
-// them with the merge kernel.
+// Shared by the per-partition, fused and head-range entry points: n_parts
+// ranges per sequence ([n_parts][B] begin / end), result (merged over the
+// ranges) into the rows of kv heads [g0, g0 + ng) of out / lse.  The plan and
+// the workspace layout are those of the sub-problem made of those heads alone
+// (dims with ng kv heads and ng x G query heads), so a head-range call does
+// exactly what the full call does on a cache holding only its heads.  Chunked
+// plans leave chunk partials in the workspace and merge them with the merge
+// kernel.
 bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
                           const int32_t* block_table, const int32_t* kv_range_begin, const int32_t* kv_range_end,
                           int n_parts, int g0, int ng, float* out, float* lse, void* workspace,
                           size_t workspace_bytes, void* stream) {
-  Plan plan = make_plan(d);
-  const WorkspaceLayout ws = layout_for(d, plan);
+  const int G = d->num_q_heads / d->num_kv_heads;
+  bana_dims sub = *d;
+  sub.num_kv_heads = ng;
+  sub.num_q_heads = ng * G;
+  Plan plan = make_plan(&sub);
+  const WorkspaceLayout ws = layout_for(&sub, plan);
   if (ws.total > 0 && (workspace == nullptr || workspace_bytes < ws.total)) {
     if (plan.balanced) {  // the chunked plan's launch shape, unsplit
-      bana_dims chunked = *d;
-      chunked.plan_hint = 1;
-      plan = make_plan(&chunked);
+      sub.plan_hint = 1;
+      plan = make_plan(&sub);
     }
     plan.nc = 1;
   }
@@ -246,14 +253,23 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
   a.B = d->batch;
   a.Hq = d->num_q_heads;
   a.Hkv = d->num_kv_heads;
-  a.G = d->num_q_heads / d->num_kv_heads;
+  a.G = G;
   a.max_blocks = d->max_blocks_per_seq;
   a.g0 = g0;
   a.ng = ng;
   a.nc = plan.nc;
   a.cmin = plan.cmin;
+  // Workspace partials hold the call's heads only; merged rows go to their place in out / lse.
+  a.out_hq = ng * G;
+  a.out_h0 = g0 * G;
+  bana::MergeRows m;
+  m.B = d->batch;
+  m.hn = ng * G;
+  m.in_hq = ng * G;
+  m.in_h0 = 0;
+  m.out_hq = d->num_q_heads;
+  m.out_h0 = g0 * G;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int64_t rows = (int64_t)d->batch * d->num_q_heads;
   if (plan.balanced) {
     char* base = static_cast<char*>(workspace);
     float* ws_out = reinterpret_cast<float*>(base + ws.out);
@@ -263,22 +279,23 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
     a.lse = ws_lse;
     hipError_t e = bana::launch_balanced_attn(a, prefix, plan.K, s);
     if (e != hipSuccess) return device_status(e);
-    return device_status(bana::launch_merge_pieces(ws_out, ws_lse, prefix, plan.K, d->batch, d->num_q_heads,
-                                                   g0 * a.G, ng * a.G, out, lse, s));
+    return device_status(bana::launch_merge_pieces(ws_out, ws_lse, prefix, plan.K, m, out, lse, s));
   }
   if (plan.nc == 1) {
     a.out = out;
     a.lse = lse;
+    a.out_hq = d->num_q_heads;
+    a.out_h0 = 0;
     return device_status(bana::launch_partial_attn(a, plan.waves, s));
   }
-  float* ws_out = static_cast<float*>(workspace);
-  float* ws_lse = ws_out + (size_t)plan.nc * rows * kHeadDim;
+  char* base = static_cast<char*>(workspace);
+  float* ws_out = reinterpret_cast<float*>(base + ws.out);
+  float* ws_lse = reinterpret_cast<float*>(base + ws.lse);
   a.out = ws_out;
   a.lse = ws_lse;
   hipError_t e = bana::launch_partial_attn(a, plan.waves, s);
   if (e != hipSuccess) return device_status(e);
-  return device_status(bana::launch_merge(ws_out, ws_lse, plan.nc, d->batch, d->num_q_heads, g0 * a.G, ng * a.G, out,
-                                          lse, s));
+  return device_status(bana::launch_merge(ws_out, ws_lse, plan.nc, m, out, lse, s));
 }
 
 }  // namespace
@@ -336,7 +353,6 @@ bana_status bana_decode_attn_heads(const bana_dims* d, const void* q, const void
       (workspace != nullptr && !aligned16(workspace)))
     return BANA_ERR_INVALID;
   if (kv_head_begin == kv_head_end) return BANA_OK;
-  // The plan comes from the full dims, so every head is computed exactly as by the full call.
   return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, 1, kv_head_begin,
                        kv_head_end - kv_head_begin, out, lse, workspace, workspace_bytes, stream);
 }
@@ -348,8 +364,15 @@ bana_status bana_merge_partials(const bana_dims* d, const float* out_partials, c
   if (d->head_dim != kHeadDim || (int64_t)d->batch * d->num_q_heads >= kMaxRows) return BANA_ERR_UNSUPPORTED;
   if (!out_partials || !lses || !out || n_parts < 1) return BANA_ERR_INVALID;
   if (!aligned16(out_partials) || !aligned16(out)) return BANA_ERR_INVALID;
-  return device_status(bana::launch_merge(out_partials, lses, n_parts, d->batch, d->num_q_heads, 0, d->num_q_heads, out,
-                                          lse_out, static_cast<hipStream_t>(stream)));
+  bana::MergeRows m;
+  m.B = d->batch;
+  m.hn = d->num_q_heads;
+  m.in_hq = d->num_q_heads;
+  m.in_h0 = 0;
+  m.out_hq = d->num_q_heads;
+  m.out_h0 = 0;
+  return device_status(bana::launch_merge(out_partials, lses, n_parts, m, out, lse_out,
+                                          static_cast<hipStream_t>(stream)));
 }
 
 bana_status bana_migrate_kv_blocks(const bana_dims* d, const void* src_k_cache, const void* src_v_cache,

@@ -16,12 +16,16 @@ struct PartialArgs {
   const int32_t* end;       // [n_parts][B]
   int n_parts;              // ranges per sequence, 1..64
   const int32_t* seq_order; // optional [B] dispatch order of sequences (NULL: natural)
-  float* out;               // nc == 1: final output [B][Hq][128]; nc > 1: chunk partials [nc][B][Hq][128]
-  float* lse;               // nc == 1: final lse [B][Hq];               nc > 1: chunk lses [nc][B][Hq]
+  float* out;               // nc == 1: final output [B][Hq][128]; nc > 1: chunk partials [nc][B][out_hq][128]
+  float* lse;               // nc == 1: final lse [B][Hq];               nc > 1: chunk lses [nc][B][out_hq]
   int B, Hq, Hkv, G, max_blocks;
   int g0, ng;  // kv heads [g0, g0 + ng) of this launch
   int nc;    // chunks per (sequence, kv head)
   int cmin;  // minimum blocks per chunk
+  // Destination rows: query head h of sequence b (chunk or piece slot c) goes to row
+  // (c * B + b) * out_hq + h - out_h0 of out / lse.  Final output: out_hq = Hq, out_h0 = 0;
+  // workspace partials of a kv-head range hold only its heads: out_hq = ng * G, out_h0 = g0 * G.
+  int out_hq, out_h0;
 };
 
 // Partial attention: one workgroup of `waves` wavefronts per (chunk, sequence, kv head).
@@ -31,18 +35,26 @@ constexpr int kBalancedWaves = 8;       // wavefronts per workgroup of the balan
 constexpr int kMaxBalancedBatch = 64;  // one sequence per lane of the in-kernel schedule
 
 // Balanced launch: K wavefronts per kv head, each over an equal interval of the call's virtual
-// blocks; a.out / a.lse are piece buffers [K + B][Hq][128] / [K + B][Hq]; prefix [B + 1]
+// blocks; a.out / a.lse are piece buffers [K + B][out_hq][128] / [K + B][out_hq]; prefix [B + 1]
 // receives the block-count prefix sums over sequences (for the merge).
 hipError_t launch_balanced_attn(const PartialArgs& a, int32_t* prefix, int K, hipStream_t stream);
 
-// Merge of the balanced launch's pieces into out / lse_out [B][Hq] rows of heads [h0, h0 + hn).
-hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, int64_t B,
-                               int Hq, int h0, int hn, float* out, float* lse_out, hipStream_t stream);
+// Rows of a merge: hn heads of each of B sequences.  Head i of sequence b is row
+// b * in_hq + in_h0 + i of every part (parts are [n_parts][B][in_hq]) and row
+// b * out_hq + out_h0 + i of out / lse_out.
+struct MergeRows {
+  int64_t B;
+  int hn, in_hq, in_h0, out_hq, out_h0;
+};
 
-// Log-sum-exp merge of n_parts partials over the rows (b, h) of B sequences x Hq heads restricted
-// to heads [h0, h0 + hn): partials are [n_parts][B][Hq][128] / [n_parts][B][Hq], outputs [B][Hq][128].
-hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn,
-                        float* out, float* lse_out, hipStream_t stream);
+// Merge of the balanced launch's pieces (slots [K + B][in_hq]) into out / lse_out.
+hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, MergeRows m,
+                               float* out, float* lse_out, hipStream_t stream);
+
+// Log-sum-exp merge of n_parts partials ([n_parts][B][in_hq][128] / [n_parts][B][in_hq]) into out / lse_out.
+// Kernel and summation order depend only on n_parts and B x hn.
+hipError_t launch_merge(const float* outs, const float* lses, int n_parts, MergeRows m, float* out, float* lse_out,
+                        hipStream_t stream);
 
 // Copy of the K/V tiles (all kv heads) of logical blocks [blk_begin[b], blk_end[b]) from the
 // src pool (src_table) to the dst pool (dst_table); grid covers max_migrated_blocks per sequence.

@@ -22,8 +22,7 @@
 //    relative to its own max and the KP groups are combined through LDS,
 //    rescaled to the common max (the same log-sum-exp algebra once more).
 // The part-to-group assignment and every summation order depend only on
-// n_parts and the total row count, so results are deterministic, and a merge
-// restricted to a range of heads gives the same bits as the full merge.
+// n_parts and the number of merged rows, so results are deterministic.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -39,15 +38,16 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // too (their rows lie inside the partial buffer) but never enter a sum.
 template <int NP>
 __global__ __launch_bounds__(256) void merge_few_kernel(const float* __restrict__ outs,
-                                                        const float* __restrict__ lses, int n_parts, int64_t B,
-                                                        int Hq, int h0, int hn, float* __restrict__ out,
-                                                        float* __restrict__ lse_out) {
+                                                        const float* __restrict__ lses, int n_parts, MergeRows mr,
+                                                        float* __restrict__ out, float* __restrict__ lse_out) {
   const int t = threadIdx.x;
   const int d4 = t & 31;
   const int64_t r = (int64_t)blockIdx.x * 8 + (t >> 5);
-  if (r >= B * hn) return;
-  const int64_t rows = B * Hq;
-  const int64_t row = (r / hn) * Hq + h0 + r % hn;
+  if (r >= mr.B * mr.hn) return;
+  const int64_t rows = mr.B * mr.in_hq;
+  const int64_t b = r / mr.hn, i = r % mr.hn;
+  const int64_t row = b * mr.in_hq + mr.in_h0 + i;
+  const int64_t orow = b * mr.out_hq + mr.out_h0 + i;
   float l[NP];
   f32x4 o[NP];
 #pragma unroll
@@ -61,10 +61,10 @@ __global__ __launch_bounds__(256) void merge_few_kernel(const float* __restrict_
 #pragma unroll
   for (int p = 0; p < NP; ++p)
     if (p < n_parts) M = fmaxf(M, l[p]);
-  f32x4* dst = reinterpret_cast<f32x4*>(out + row * 128) + d4;
+  f32x4* dst = reinterpret_cast<f32x4*>(out + orow * 128) + d4;
   if (M == -INFINITY) {
     *dst = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (lse_out != nullptr && d4 == 0) lse_out[row] = -INFINITY;
+    if (lse_out != nullptr && d4 == 0) lse_out[orow] = -INFINITY;
     return;
   }
   float wsum = 0.f;
@@ -78,24 +78,23 @@ __global__ __launch_bounds__(256) void merge_few_kernel(const float* __restrict_
     }
   }
   *dst = acc * (1.0f / wsum);
-  if (lse_out != nullptr && d4 == 0) lse_out[row] = M + logf(wsum);
+  if (lse_out != nullptr && d4 == 0) lse_out[orow] = M + logf(wsum);
 }
 
 constexpr int kUnroll = 4;  // partial rows in flight per lane
 
 // Any number of parts.  Group k (of KP) of a row takes parts k, k + KP, ...;
-// its q-th part is p = k + KP q.  Part p of output row `row` is row
-// base + p * prow of the part buffers: base = row and prow = B x Hq for
-// partials [n_parts][B][Hq]; for the balanced launch's pieces, base is the
-// row's head in the sequence's first piece slot and prow = Hq (the slots of
-// a sequence's pieces are consecutive), and the part count comes from the
-// block-count prefix sums (pieces = intervals of S blocks that overlap the
-// sequence's blocks [prefix[b], prefix[b + 1])).
+// its q-th part is p = k + KP q.  Part p of merged row r (head i of sequence
+// b) is row base + p * prow of the part buffers: base = b * in_hq + in_h0 + i
+// and prow = B x in_hq for partials [n_parts][B][in_hq]; for the balanced
+// launch's pieces, base is the head's row in the sequence's first piece slot
+// and prow = in_hq (the slots of a sequence's pieces are consecutive), and the
+// part count comes from the block-count prefix sums (pieces = intervals of S
+// blocks that overlap the sequence's blocks [prefix[b], prefix[b + 1])).
 template <int KP, bool PIECES>
 __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict__ outs,
-                                                         const float* __restrict__ lses, int n_parts, int64_t B,
-                                                         int Hq, int h0, int hn, float* __restrict__ out,
-                                                         float* __restrict__ lse_out,
+                                                         const float* __restrict__ lses, int n_parts, MergeRows mr,
+                                                         float* __restrict__ out, float* __restrict__ lse_out,
                                                          const int32_t* __restrict__ prefix, int K) {
   constexpr int R = 256 / (32 * KP);  // rows per workgroup
   __shared__ f32x4 sm_acc[KP > 1 ? R * KP * 32 : 1];
@@ -106,23 +105,24 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
   const int k = (t >> 5) % KP;
   const int rl = t / (32 * KP);
   const int64_t r = (int64_t)blockIdx.x * R + rl;  // row among the B x hn merged rows
-  const bool live = r < B * hn;
-  const int64_t row = live ? (r / hn) * Hq + h0 + r % hn : 0;
-  int64_t base = row;
-  int64_t prow = B * Hq;
+  const bool live = r < mr.B * mr.hn;
+  const int64_t b = live ? r / mr.hn : 0;
+  const int64_t i = live ? r % mr.hn : 0;
+  const int64_t dst_row = b * mr.out_hq + mr.out_h0 + i;
+  int64_t base = b * mr.in_hq + mr.in_h0 + i;
+  int64_t prow = mr.B * mr.in_hq;
   int n = n_parts;
   if (PIECES) {
     n = 0;
-    prow = Hq;
+    prow = mr.in_hq;
     if (live) {
-      const int64_t b = r / hn;
-      const int p0 = prefix[b], p1 = prefix[b + 1], U = prefix[B];
+      const int p0 = prefix[b], p1 = prefix[b + 1], U = prefix[mr.B];
       const int64_t S = U > K ? ((int64_t)U + K - 1) / K : 1;
       if (p1 > p0) {  // slots clamped to [b, K + b): prefix sums from another call cannot reach outside
         const int64_t first = min(max((int64_t)p0 / S, (int64_t)0), (int64_t)K - 1);
         const int64_t last = min(max((int64_t)(p1 - 1) / S, first), (int64_t)K - 1);
         n = (int)(last - first + 1);
-        base = (first + b) * Hq + h0 + r % hn;
+        base = (first + b) * mr.in_hq + mr.in_h0 + i;
       }
     }
   }
@@ -194,56 +194,56 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
     }
   }
   if (!live) return;
-  f32x4* dst = reinterpret_cast<f32x4*>(out + row * 128) + d4;
+  f32x4* dst = reinterpret_cast<f32x4*>(out + dst_row * 128) + d4;
   if (M == -INFINITY) {
     *dst = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (lse_out != nullptr && d4 == 0) lse_out[row] = -INFINITY;
+    if (lse_out != nullptr && d4 == 0) lse_out[dst_row] = -INFINITY;
     return;
   }
   *dst = acc * (1.0f / wsum);
-  if (lse_out != nullptr && d4 == 0) lse_out[row] = M + logf(wsum);
+  if (lse_out != nullptr && d4 == 0) lse_out[dst_row] = M + logf(wsum);
 }
 
 template <int KP, bool PIECES = false>
-hipError_t launch_many(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn,
-                       float* out, float* lse_out, hipStream_t stream, const int32_t* prefix = nullptr,
-                       int K = 0) {
+hipError_t launch_many(const float* outs, const float* lses, int n_parts, const MergeRows& m, float* out,
+                       float* lse_out, hipStream_t stream, const int32_t* prefix = nullptr, int K = 0) {
   constexpr int R = 256 / (32 * KP);
-  const int64_t rows = B * hn;
+  const int64_t rows = m.B * m.hn;
   const unsigned grid = (unsigned)((rows + R - 1) / R);
-  hipLaunchKernelGGL((merge_many_kernel<KP, PIECES>), dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, B, Hq,
-                     h0, hn, out, lse_out, prefix, K);
+  hipLaunchKernelGGL((merge_many_kernel<KP, PIECES>), dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, m, out,
+                     lse_out, prefix, K);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_merge(const float* outs, const float* lses, int n_parts, int64_t B, int Hq, int h0, int hn,
-                        float* out, float* lse_out, hipStream_t stream) {
-  if (B * hn == 0) return hipSuccess;
+hipError_t launch_merge(const float* outs, const float* lses, int n_parts, MergeRows m, float* out, float* lse_out,
+                        hipStream_t stream) {
+  const int64_t rows = m.B * m.hn;
+  if (rows == 0) return hipSuccess;
   if (n_parts <= 4) {
-    hipLaunchKernelGGL(merge_few_kernel<4>, dim3((unsigned)((B * hn + 7) / 8)), dim3(256), 0, stream, outs, lses,
-                       n_parts, B, Hq, h0, hn, out, lse_out);
+    hipLaunchKernelGGL(merge_few_kernel<4>, dim3((unsigned)((rows + 7) / 8)), dim3(256), 0, stream, outs, lses,
+                       n_parts, m, out, lse_out);
     return hipGetLastError();
   }
   // With enough rows to fill the GPU, one thread group per row streams best.
   // With few rows (long ranges of few sequences), spread a row's parts over
-  // up to 8 thread groups, at least 4 parts each.  The choice uses the full
-  // row count B x Hq so that a head range merges exactly like the full call.
-  if (B * Hq < 4096) {
-    if (n_parts >= 32) return launch_many<8>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
-    if (n_parts >= 16) return launch_many<4>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
-    if (n_parts >= 8) return launch_many<2>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
+  // up to 8 thread groups, at least 4 parts each.
+  if (rows < 4096) {
+    if (n_parts >= 32) return launch_many<8>(outs, lses, n_parts, m, out, lse_out, stream);
+    if (n_parts >= 16) return launch_many<4>(outs, lses, n_parts, m, out, lse_out, stream);
+    if (n_parts >= 8) return launch_many<2>(outs, lses, n_parts, m, out, lse_out, stream);
   }
-  return launch_many<1>(outs, lses, n_parts, B, Hq, h0, hn, out, lse_out, stream);
+  return launch_many<1>(outs, lses, n_parts, m, out, lse_out, stream);
 }
 
-hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, int64_t B,
-                               int Hq, int h0, int hn, float* out, float* lse_out, hipStream_t stream) {
-  if (B * hn == 0) return hipSuccess;
+hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, MergeRows m,
+                               float* out, float* lse_out, hipStream_t stream) {
+  const int64_t rows = m.B * m.hn;
+  if (rows == 0) return hipSuccess;
   // Few rows come with long sequences, hence many pieces per row: spread them over 8 thread groups.
-  if (B * Hq < 4096) return launch_many<8, true>(outs, lses, 0, B, Hq, h0, hn, out, lse_out, stream, prefix, K);
-  return launch_many<1, true>(outs, lses, 0, B, Hq, h0, hn, out, lse_out, stream, prefix, K);
+  if (rows < 4096) return launch_many<8, true>(outs, lses, 0, m, out, lse_out, stream, prefix, K);
+  return launch_many<1, true>(outs, lses, 0, m, out, lse_out, stream, prefix, K);
 }
 
 }  // namespace bana

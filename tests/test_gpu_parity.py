@@ -407,24 +407,41 @@ def test_migration_bit_exact_and_attention_unchanged(name, part):
 
 
 @pytest.mark.parametrize("name,part,split", [("tiny", 0, 1), ("llama3_8b", 0, 3), ("long", 0, 5), ("mixed", 1, 4)])
-def test_head_split_concatenates_to_unsplit_bit_exact(name, part, split):
-    """Head partitions (the literal head-dimension split): complementary kv-head ranges give the
-    full partition result bit for bit, and a call leaves the rows of other heads untouched."""
+def test_head_split_equals_the_call_on_a_cache_of_those_heads(name, part, split):
+    """Head partitions (the literal head-dimension split): a kv-head range call gives, bit for bit, what
+    the partial call gives on a cache holding only those heads (the device they migrate to), writes
+    only its own rows, and complementary ranges together match the oracle."""
     w = _workload(name)
     dw = DeviceWorkload(w)
-    op, lp, _, _ = dw.results()
-    B, Hq, G = w.batch, w.num_q_heads, w.group
+    B, Hq, Hkv, G = w.batch, w.num_q_heads, w.num_kv_heads, w.group
     out = torch.full((B, Hq, 128), float("nan"), dtype=torch.float32, device="cuda")
     lse = torch.full((B, Hq), float("nan"), dtype=torch.float32, device="cuda")
-    args = (dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin[part], dw.kv_end[part])
-    _log(f"[heads] {name} part {part} split at kv head {split}")
-    bana.bana_decode_attn_heads(*args, 0, split, out, lse, workspace=dw.workspace, dims=dw.dims[part])
-    o = out.cpu().numpy()
-    assert np.all(np.isnan(o[:, split * G:])) and np.all(np.isnan(lse.cpu().numpy()[:, split * G:]))
-    assert np.array_equal(o[:, :split * G], op[part][:, :split * G])
-    bana.bana_decode_attn_heads(*args, split, w.num_kv_heads, out, lse, workspace=dw.workspace, dims=dw.dims[part])
-    assert np.array_equal(out.cpu().numpy(), op[part])
-    assert np.array_equal(lse.cpu().numpy(), lp[part])
+    begin, end = dw.kv_begin[part], dw.kv_end[part]
+    for g0, g1 in ((0, split), (split, Hkv)):
+        _log(f"[heads] {name} part {part} kv heads [{g0}, {g1})")
+        sub = bana.head_range_dims(dw.dims[part], g0, g1)
+        ws = torch.empty(max(256, bana.bana_decode_attn_workspace_bytes(sub)), dtype=torch.uint8, device="cuda")
+        bana.bana_decode_attn_heads(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, begin, end, g0, g1,
+                                    out, lse, workspace=ws, dims=dw.dims[part])
+        if g0 == 0:
+            o = out.cpu().numpy()
+            assert np.all(np.isnan(o[:, g1 * G:])) and np.all(np.isnan(lse.cpu().numpy()[:, g1 * G:]))
+        q_s = dw.q[:, g0 * G:g1 * G].contiguous()
+        k_s = dw.k_cache[:, g0:g1].contiguous()
+        v_s = dw.v_cache[:, g0:g1].contiguous()
+        o_s = torch.empty((B, (g1 - g0) * G, 128), dtype=torch.float32, device="cuda")
+        l_s = torch.empty((B, (g1 - g0) * G), dtype=torch.float32, device="cuda")
+        ws2 = torch.empty_like(ws)
+        bana.bana_decode_attn_partial(q_s, k_s, v_s, dw.block_table, dw.seq_lens, begin, end, o_s, l_s,
+                                      workspace=ws2, dims=sub)
+        assert np.array_equal(out[:, g0 * G:g1 * G].cpu().numpy(), o_s.cpu().numpy())
+        assert np.array_equal(lse[:, g0 * G:g1 * G].cpu().numpy(), l_s.cpu().numpy())
+    ro, rl = oracle.workload_partials(w)
+    fin = np.isfinite(rl[part])
+    o, l = out.cpu().numpy(), lse.cpu().numpy()
+    _check_out(o[fin], ro[part][fin], f"{name} head-split out")
+    assert np.all(o[~fin] == 0.0)
+    _check_lse(l, rl[part], f"{name} head-split lse")
 
 
 def test_hip_graph_capture_and_replay():
