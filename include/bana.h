@@ -146,8 +146,11 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
  * of the range's query heads (h with h / G in the kv-head range) of out / lse
  * are written; other rows are left untouched.  With head partitions the
  * "merge" is the concatenation of rows: calls over complementary kv-head
- * ranges give the full result (up to float rounding order, as the full call
- * may plan its launch differently).  An empty kv-head range does nothing.
+ * ranges give the full result, up to float rounding order as the full call
+ * may plan its launch differently; with the launch shape fixed by
+ * waves_hint and chunks_hint (both non-zero, chunks_hint <= 4) the plan does
+ * not depend on the number of heads and the concatenation equals the full
+ * call bit for bit.  An empty kv-head range does nothing.
  * workspace: as for bana_decode_attn_partial, sized by
  * bana_decode_attn_workspace_bytes of the sub-problem's dims.  Other
  * arguments and errors as for bana_decode_attn_partial; a kv-head range

@@ -410,7 +410,8 @@ def test_migration_bit_exact_and_attention_unchanged(name, part):
 def test_head_split_equals_the_call_on_a_cache_of_those_heads(name, part, split):
     """Head partitions (the literal head-dimension split): a kv-head range call gives, bit for bit, what
     the partial call gives on a cache holding only those heads (the device they migrate to), writes
-    only its own rows, and complementary ranges together match the oracle."""
+    only its own rows, and complementary ranges together match the oracle; with a fixed launch shape
+    they concatenate to the unsplit call bit for bit."""
     w = _workload(name)
     dw = DeviceWorkload(w)
     B, Hq, Hkv, G = w.batch, w.num_q_heads, w.num_kv_heads, w.group
@@ -442,6 +443,24 @@ def test_head_split_equals_the_call_on_a_cache_of_those_heads(name, part, split)
     _check_out(o[fin], ro[part][fin], f"{name} head-split out")
     assert np.all(o[~fin] == 0.0)
     _check_lse(l, rl[part], f"{name} head-split lse")
+
+    # With the launch shape fixed by the hints, the plan no longer depends on the number of heads:
+    # complementary head ranges then concatenate to the unsplit call bit for bit.
+    lens = w.kv_end[part].astype(np.int64) - w.kv_begin[part]
+    fixed = bana.make_dims(B, Hq, Hkv, w.max_blocks_per_seq, w.num_blocks, max_range_tokens=int(lens.max()),
+                           total_range_tokens=int(lens.sum()), waves_hint=4, chunks_hint=3)
+    ws = torch.empty(max(256, bana.bana_decode_attn_workspace_bytes(fixed)), dtype=torch.uint8, device="cuda")
+    full_o = torch.empty((B, Hq, 128), dtype=torch.float32, device="cuda")
+    full_l = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+    bana.bana_decode_attn_partial(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, begin, end, full_o,
+                                  full_l, workspace=ws, dims=fixed)
+    out.fill_(float("nan"))
+    lse.fill_(float("nan"))
+    for g0, g1 in ((0, split), (split, Hkv)):
+        bana.bana_decode_attn_heads(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, begin, end, g0, g1,
+                                    out, lse, workspace=ws, dims=fixed)
+    assert np.array_equal(out.cpu().numpy(), full_o.cpu().numpy())
+    assert np.array_equal(lse.cpu().numpy(), full_l.cpu().numpy())
 
 
 def test_hip_graph_capture_and_replay():
