@@ -172,20 +172,12 @@ def bana_decode_attn_partial(q, k_cache, v_cache, block_table, seq_lens, kv_rang
                              out_partial, lse, workspace: Optional[torch.Tensor] = None, stream=None,
                              dims: Optional[bana_dims] = None, max_range_tokens: int = 0) -> None:
     """Partial attention of one partition; see ``bana_decode_attn_partial`` in include/bana.h."""
-    if q.dim() != 3 or k_cache.dim() != 5:
-        raise ValueError("q must be [B, Hq, D] and k_cache [num_blocks, Hkv, D / 8, block_size, 8]")
-    B, Hq, D = q.shape
-    nb, Hkv, _, bs, _ = k_cache.shape
-    _need(q, "q", torch.bfloat16)
-    _need(k_cache, "k_cache", torch.bfloat16, (nb, Hkv, D // 8, bs, 8))
-    _need(v_cache, "v_cache", torch.bfloat16, (nb, Hkv, D, bs))
-    _need(block_table, "block_table", torch.int32)
-    if block_table.dim() != 2 or block_table.shape[0] != B:
-        raise ValueError("block_table must be [B, max_blocks_per_seq]")
-    for name, t in (("seq_lens", seq_lens), ("kv_range_begin", kv_range_begin), ("kv_range_end", kv_range_end)):
-        _need(t, name, torch.int32, (B,))
+    B, Hq, D = _check_attn_inputs(q, k_cache, v_cache, block_table, seq_lens)
+    _need(kv_range_begin, "kv_range_begin", torch.int32, (B,))
+    _need(kv_range_end, "kv_range_end", torch.int32, (B,))
     _need(out_partial, "out_partial", torch.float32, (B, Hq, D))
     _need(lse, "lse", torch.float32, (B, Hq))
+    _same_device(q, kv_range_begin, kv_range_end, out_partial, lse, workspace)
     ws_bytes = 0
     if workspace is not None:
         _need(workspace, "workspace", workspace.dtype)
@@ -213,7 +205,18 @@ def _check_attn_inputs(q, k_cache, v_cache, block_table, seq_lens):
     if block_table.dim() != 2 or block_table.shape[0] != B:
         raise ValueError("block_table must be [B, max_blocks_per_seq]")
     _need(seq_lens, "seq_lens", torch.int32, (B,))
+    _same_device(q, k_cache, v_cache, block_table, seq_lens)
     return B, Hq, D
+
+
+def _same_device(*tensors) -> None:
+    """Every tensor of a call on one device, the current one (the library launches there)."""
+    devs = {t.device for t in tensors if t is not None}
+    if len(devs) != 1:
+        raise ValueError(f"tensors of one call are on several devices: {sorted(map(str, devs))}")
+    dev = devs.pop()
+    if dev.index is not None and dev.index != torch.cuda.current_device():
+        raise ValueError(f"tensors are on {dev}, but the current device is cuda:{torch.cuda.current_device()}")
 
 
 def bana_decode_attn_fused(q, k_cache, v_cache, block_table, seq_lens, kv_range_begin, kv_range_end, out, lse_out,
@@ -228,6 +231,7 @@ def bana_decode_attn_fused(q, k_cache, v_cache, block_table, seq_lens, kv_range_
     _need(kv_range_end, "kv_range_end", torch.int32, (n, B))
     _need(out, "out", torch.float32, (B, Hq, D))
     _need(lse_out, "lse_out", torch.float32, (B, Hq))
+    _same_device(q, kv_range_begin, kv_range_end, out, lse_out, workspace)
     ws_bytes = 0
     if workspace is not None:
         _need(workspace, "workspace", workspace.dtype)
@@ -255,6 +259,7 @@ def bana_decode_attn_heads(q, k_cache, v_cache, block_table, seq_lens, kv_range_
     _need(kv_range_end, "kv_range_end", torch.int32, (B,))
     _need(out, "out", torch.float32, (B, Hq, D))
     _need(lse, "lse", torch.float32, (B, Hq))
+    _same_device(q, kv_range_begin, kv_range_end, out, lse, workspace)
     ws_bytes = 0
     if workspace is not None:
         _need(workspace, "workspace", workspace.dtype)
@@ -280,6 +285,7 @@ def bana_merge_partials(out_partials, lses, out, lse_out: Optional[torch.Tensor]
     _need(out, "out", torch.float32, (B, Hq, D))
     if lse_out is not None:
         _need(lse_out, "lse_out", torch.float32, (B, Hq))
+    _same_device(out_partials, lses, out, lse_out)
     dims = bana_dims(B, Hq, 1, D, BLOCK_SIZE, 1, 1, 0, 0, 0, 0, 0)
     st = lib().bana_merge_partials(ctypes.byref(dims), _ptr(out_partials), _ptr(lses), n, _ptr(out), _ptr(lse_out),
                                    _stream(stream))
@@ -303,6 +309,7 @@ def bana_migrate_kv_blocks(src_k, src_v, src_table, dst_k, dst_v, dst_table, blk
     _need(dst_table, "dst_table", torch.int32, (B, mb))
     _need(blk_begin, "blk_begin", torch.int32, (B,))
     _need(blk_end, "blk_end", torch.int32, (B,))
+    _same_device(src_k, src_v, src_table, dst_k, dst_v, dst_table, blk_begin, blk_end)
     dims = bana_dims(B, Hkv, Hkv, HEAD_DIM, bs, mb, nb, max_range_tokens, 0, 0, 0, 0)
     st = lib().bana_migrate_kv_blocks(ctypes.byref(dims), _ptr(src_k), _ptr(src_v), _ptr(src_table), _ptr(dst_k),
                                       _ptr(dst_v), _ptr(dst_table), nbd, _ptr(blk_begin), _ptr(blk_end),
@@ -323,6 +330,7 @@ def bana_validate_ranges(block_table, seq_lens, kv_range_begin, kv_range_end, nu
     _need(kv_range_begin, "kv_range_begin", torch.int32, (n, B))
     _need(kv_range_end, "kv_range_end", torch.int32, (n, B))
     _need(result, "result", torch.int32, (1,))
+    _same_device(block_table, seq_lens, kv_range_begin, kv_range_end, result)
     dims = bana_dims(B, 1, 1, HEAD_DIM, BLOCK_SIZE, mb, num_blocks, 0, 0, 0, 0, 0)
     st = lib().bana_validate_ranges(ctypes.byref(dims), _ptr(block_table), _ptr(seq_lens), _ptr(kv_range_begin),
                                     _ptr(kv_range_end), n, _ptr(result), _stream(stream))
@@ -338,6 +346,7 @@ def bana_debug_kv_rows(block_table, kv_range_begin, kv_range_end, num_blocks: in
     _need(kv_range_begin, "kv_range_begin", torch.int32, (B,))
     _need(kv_range_end, "kv_range_end", torch.int32, (B,))
     _need(rows_out, "rows_out", torch.int64, (B, num_kv_heads, mb * BLOCK_SIZE))
+    _same_device(block_table, kv_range_begin, kv_range_end, rows_out)
     dims = bana_dims(B, num_kv_heads, num_kv_heads, HEAD_DIM, BLOCK_SIZE, mb, num_blocks, 0, 0, 0, 0, 0)
     st = lib().bana_debug_kv_rows(ctypes.byref(dims), _ptr(block_table), _ptr(kv_range_begin), _ptr(kv_range_end),
                                   _ptr(rows_out), _stream(stream))
@@ -362,6 +371,7 @@ def bana_debug_gather_read(k_cache, v_cache, block_table, kv_range_begin, kv_ran
     _need(kv_range_begin, "kv_range_begin", torch.int32, (n, B))
     _need(kv_range_end, "kv_range_end", torch.int32, (n, B))
     _need(sink, "sink", torch.int32, (B, Hkv))
+    _same_device(k_cache, v_cache, block_table, kv_range_begin, kv_range_end, sink)
     dims = bana_dims(B, Hkv, Hkv, D8 * 8, bs, mb, nb, 0, 0, 0, 0, 0)
     st = lib().bana_debug_gather_read(ctypes.byref(dims), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
                                       _ptr(kv_range_begin), _ptr(kv_range_end), n, _ptr(sink), _stream(stream))
@@ -379,6 +389,7 @@ def bana_debug_stream_read(buf: torch.Tensor, sink: torch.Tensor, stream=None) -
     if not isinstance(buf, torch.Tensor) or buf.device.type != "cuda" or not buf.is_contiguous():
         raise ValueError("buf must be a contiguous device tensor")
     _need(sink, "sink", torch.int32)
+    _same_device(buf, sink)
     nbytes = buf.numel() * buf.element_size()
     st = lib().bana_debug_stream_read(_ptr(buf), nbytes, sink.numel(), _ptr(sink), _stream(stream))
     if st != BANA_OK:

@@ -74,14 +74,12 @@ class LayerPipeline:
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device) if ws else None
         self.out = torch.empty((self.L, B, Hq, bana.HEAD_DIM), dtype=torch.float32, device=self.device)
         self.lse = torch.empty((self.L, B, Hq), dtype=torch.float32, device=self.device)
-        # Fetches and stores share one copy stream by default: measured on MI355X, giving the two
-        # channels streams of their own stalled the issuing host thread (5x slower per layer),
-        # while one copy stream already hides both transfers under the attention of the layer.
+        # Fetches and stores share one copy stream by default: measured on MI355X (llama3_8b layer),
+        # giving the two channels streams of their own took 0.26 ms per layer against 0.23 ms.
         self.s_comp = compute_stream or torch.cuda.current_stream(self.device)
         self.s_h2d = torch.cuda.Stream(device=self.device)
         self.s_d2h = torch.cuda.Stream(device=self.device) if separate_copy_streams else self.s_h2d
         self.stage_ms = None
-
 
         # Validate the attention arguments once through the checked binding, then keep raw
         # argument lists so the per-layer host work stays far below the per-layer GPU work.

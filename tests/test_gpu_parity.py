@@ -371,6 +371,14 @@ def test_non_default_stream_and_binding_checks():
     with pytest.raises(ValueError):
         bana.bana_decode_attn_fused(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin,
                                     dw.kv_end, dw.fused_out, dw.fused_lse, dims=bad)
+    # host memory where device memory is expected is refused before any launch
+    with pytest.raises(ValueError):
+        bana.bana_decode_attn_partial(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin[0],
+                                      dw.kv_end[0], dw.out_partials[0].cpu(), dw.lses[0])
+    with pytest.raises(ValueError):
+        bana.bana_decode_attn_partial(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin[0],
+                                      dw.kv_end[0], dw.out_partials[0], dw.lses[0],
+                                      workspace=torch.empty(1 << 20, dtype=torch.uint8))
 
 
 @pytest.mark.parametrize("name,part", [("tiny", 0), ("tiny", 1), ("llama3_8b", 1), ("mixed", 1)])
