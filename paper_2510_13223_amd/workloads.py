@@ -345,6 +345,44 @@ def make_custom(
                           cfg_id=100, q_scale=q_scale, key_bias_std=key_bias_std, pool_factor=pool_factor)
 
 
+def make_shared_pool(seed: int, batch: int, num_q_heads: int, num_kv_heads: int, seq_lens, pool_blocks: int,
+                     q_bank: int = 65536, q_scale: float = 1.0) -> Workload:
+    """Very large batches over a small pool: every logical block of every sequence maps to a block
+    drawn uniformly from ``pool_blocks`` physical blocks (blocks are shared between sequences, as
+    with shared prefixes), and each (sequence, head) query row is one of ``q_bank`` N(0, 1) rows
+    drawn once.  One partition [0, seq_len) per sequence.  Host memory stays near the size of q
+    itself, so batches of a million sequences can be drawn in seconds."""
+    cfg_id = 101
+    B, Hq, Hkv, D, bs = batch, num_q_heads, num_kv_heads, HEAD_DIM, BLOCK_SIZE
+    seq_lens = np.asarray(seq_lens, dtype=np.int32)
+    nbs = (seq_lens.astype(np.int64) + bs - 1) // bs
+    mb = max(1, int(nbs.max()))
+    g = _rng(seed, cfg_id, _S_PERM)
+    table = g.integers(0, pool_blocks, size=(B, mb), dtype=np.int32)
+    table[np.arange(mb)[None, :] >= nbs[:, None]] = -1
+    bank = _gen_normal_bf16(seed, cfg_id, _S_Q, -1, (q_bank, D), scale=q_scale)
+    pick = _rng(seed, cfg_id, _S_SPLIT).integers(0, q_bank, size=B * Hq)
+    q = bank[pick].reshape(B, Hq, D)
+    kk = _gen_normal_bf16(seed, cfg_id, _S_K, 0, (pool_blocks, Hkv, bs, D))
+    vv = _gen_normal_bf16(seed, cfg_id, _S_V, 0, (pool_blocks, Hkv, bs, D))
+    k_cache = np.ascontiguousarray(kk.reshape(pool_blocks, Hkv, bs, D // K_CHUNK, K_CHUNK).transpose(0, 1, 3, 2, 4))
+    v_cache = np.ascontiguousarray(vv.transpose(0, 1, 3, 2))
+    begin = np.zeros((1, B), dtype=np.int32)
+    end = seq_lens[None, :].copy()
+    return Workload("shared_pool", seed, Hq, Hkv, q, k_cache, v_cache, table, seq_lens, begin, end,
+                    int(seq_lens.max()))
+
+
+def subset(w: Workload, seqs) -> Workload:
+    """The sequences ``seqs`` of a workload (same pools): results per sequence do not depend on the
+    other sequences of a batch, so a subset checks sampled rows of a large batch."""
+    seqs = np.asarray(seqs, dtype=np.int64)
+    return dataclasses.replace(w, q=np.ascontiguousarray(w.q[seqs]), block_table=np.ascontiguousarray(w.block_table[seqs]),
+                               seq_lens=np.ascontiguousarray(w.seq_lens[seqs]),
+                               kv_begin=np.ascontiguousarray(w.kv_begin[:, seqs]),
+                               kv_end=np.ascontiguousarray(w.kv_end[:, seqs]))
+
+
 def permute_physical(w: Workload, seed: int) -> Workload:
     """Same logical content under a different physical block placement."""
     g = _rng(seed, 1000, _S_PERM)

@@ -576,6 +576,61 @@ def test_pool_beyond_4gib_uses_64bit_offsets():
     torch.cuda.empty_cache()
 
 
+def test_million_sequences_at_the_launch_size_limits():
+    """2^20 sequences x 8 kv heads (G = 1) with uneven ranges: the plan asks for 8 wavefronts per
+    (sequence, kv head), which would pass 2^32 work-items in one launch, so the planner halves them;
+    the per-partition call, a two-range fused call and the merge run at this size, and sampled rows
+    (the two long sequences and 254 others) match the oracle."""
+    B, H = 1 << 20, 8
+    lens = np.full(B, 16, dtype=np.int32)
+    rng = np.random.default_rng(11)
+    lens[rng.integers(0, B, size=B // 8)] = 5  # ragged single blocks
+    lens[12345], lens[B - 1] = 1024, 1000        # longest / mean > 1.25: uneven, 64 blocks
+    _log(f"[1M] drawing B={B} H={H}")
+    w = W.make_shared_pool(3, B, H, H, lens, pool_blocks=4096, q_scale=1 / math.sqrt(128))
+    dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a).view(dt)).cuda()
+    q = dev(w.q, np.int16).view(torch.bfloat16)
+    k = dev(w.k_cache, np.int16).view(torch.bfloat16)
+    v = dev(w.v_cache, np.int16).view(torch.bfloat16)
+    table, sl = dev(w.block_table, np.int32), dev(w.seq_lens, np.int32)
+    begin, end = dev(w.kv_begin[0], np.int32), dev(w.kv_end[0], np.int32)
+    dims = bana.make_dims(B, H, H, w.max_blocks_per_seq, w.num_blocks, max_range_tokens=int(lens.max()),
+                          total_range_tokens=int(lens.astype(np.int64).sum()))
+    ws_bytes = bana.bana_decode_attn_workspace_bytes(dims)
+    ws = torch.empty(max(256, ws_bytes), dtype=torch.uint8, device="cuda")
+    out = torch.empty((B, H, 128), dtype=torch.float32, device="cuda")
+    lse = torch.empty((B, H), dtype=torch.float32, device="cuda")
+    _log("[1M] partial call")
+    bana.bana_decode_attn_partial(q, k, v, table, sl, begin, end, out, lse, workspace=ws, dims=dims)
+    # two ranges per sequence: [0, L/2) and [L/2, L) (the first empty for one-token halves)
+    half = (lens // 2).astype(np.int32)
+    b2 = np.stack([np.zeros(B, np.int32), half])
+    e2 = np.stack([half, lens])
+    fo = torch.empty_like(out)
+    fl = torch.empty_like(lse)
+    _log("[1M] fused call")
+    bana.bana_decode_attn_fused(q, k, v, table, sl, dev(b2, np.int32), dev(e2, np.int32), fo, fl, workspace=ws,
+                                dims=dims)
+    _log("[1M] merge of the two results")
+    mo = torch.empty_like(out)
+    ml = torch.empty_like(lse)
+    bana.bana_merge_partials(torch.stack([out, fo]), torch.stack([lse, fl]), mo, ml)
+    torch.cuda.synchronize()
+    seqs = np.unique(np.concatenate([[0, 12345, B - 1], rng.integers(0, B, size=253)]))
+    sub = W.subset(w, seqs)
+    ro, rl = oracle.workload_partials(sub)
+    idx = torch.from_numpy(seqs).cuda()
+    _check_out(out[idx].cpu().numpy(), ro[0], "1M partial out")
+    _check_lse(lse[idx].cpu().numpy(), rl[0], "1M partial lse")
+    _check_out(fo[idx].cpu().numpy(), ro[0], "1M fused out")
+    _check_lse(fl[idx].cpu().numpy(), rl[0], "1M fused lse")
+    # merging a result with itself keeps the output and adds ln 2 to the lse
+    _check_out(mo[idx].cpu().numpy(), ro[0], "1M self-merge out")
+    _check_lse(ml[idx].cpu().numpy(), rl[0] + math.log(2.0), "1M self-merge lse")
+    del q, k, v, out, fo, mo, ws
+    torch.cuda.empty_cache()
+
+
 def test_validate_ranges_codes():
     w = _workload("tiny", 0)
     dw = DeviceWorkload(w)
