@@ -843,3 +843,47 @@ def test_random_shapes_every_launch_shape(case):
     _log(f"[random {case}] B={B} Hq={Hq} Hkv={Hkv} parts={n_parts}")
     for plan in (0, 1, 2):
         _full_parity(w, plan_hint=plan)
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_random_launch_hints_and_head_ranges(case):
+    """Seeded random small workloads (up to 40 sequences, G up to 16, 1-6 ranges each) under random
+    launch hints (waves, chunks, plan, dispatch order, no workspace, no range hints), per-partition,
+    merged and fused against the oracle, plus a random kv-head range of partition 0."""
+    rng = np.random.default_rng(50000 + case)
+    B = int(rng.integers(1, 41))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    Hq = Hkv * int(rng.choice([1, 2, 3, 4, 8, 16]))
+    n_parts = int(rng.integers(1, 7))
+    maxL = int(rng.choice([64, 600, 5000]))
+    lens = [int(x) for x in rng.integers(1, maxL + 1, size=B)]
+    ranges = [[] for _ in range(n_parts)]
+    for L in lens:
+        cuts = np.sort(rng.integers(0, L + 1, size=n_parts - 1)).tolist()
+        edges = [0] + cuts + [L]
+        for p in range(n_parts):
+            ranges[p].append((edges[p], edges[p + 1]))
+    w = W.make_custom(70000 + case, B, Hq, Hkv, lens, ranges, q_scale=1 / math.sqrt(128))
+    kw = dict(waves_hint=int(rng.choice([0, 0, 1, 2, 4, 8])), chunks_hint=int(rng.choice([0, 0, 1, 2, 3, 5, 9])),
+              plan_hint=int(rng.choice([0, 0, 1, 2])), order_hints=bool(rng.integers(0, 2)),
+              use_workspace=bool(rng.integers(0, 4) > 0), range_hints=bool(rng.integers(0, 4) > 0))
+    _log(f"[hints {case}] B={B} Hq={Hq} Hkv={Hkv} parts={n_parts} maxL={maxL} {kw}")
+    dw = _full_parity(w, **kw)
+    if Hkv > 1:
+        ro, rl = oracle.workload_partials(w)
+        g0 = int(rng.integers(0, Hkv))
+        g1 = int(rng.integers(g0 + 1, Hkv + 1))
+        G = Hq // Hkv
+        sub = bana.head_range_dims(dw.dims[0], g0, g1)
+        ws = torch.empty(max(256, bana.bana_decode_attn_workspace_bytes(sub)), dtype=torch.uint8, device="cuda")
+        o = torch.full((B, Hq, 128), float("nan"), device="cuda")
+        l = torch.full((B, Hq), float("nan"), device="cuda")
+        bana.bana_decode_attn_heads(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin[0],
+                                    dw.kv_end[0], g0, g1, o, l, workspace=ws, dims=dw.dims[0])
+        o, l = o.cpu().numpy(), l.cpu().numpy()
+        hs = slice(g0 * G, g1 * G)
+        fin = np.isfinite(rl[0][:, hs])
+        _check_out(o[:, hs][fin], ro[0][:, hs][fin], "head range out")
+        assert np.all(o[:, hs][~fin] == 0.0)
+        _check_lse(l[:, hs], rl[0][:, hs], "head range lse")
+        assert np.all(np.isnan(o[:, :g0 * G])) and np.all(np.isnan(o[:, g1 * G:]))
