@@ -12,8 +12,11 @@ block 16, seq_len 4096, last 30 % of each sequence's blocks migrated ->
 
 Prints ONE JSON line.  ``value`` is the KV-read bandwidth of the whole step
 (K+V bytes of all covered tokens / step time); ``tokens_per_s`` is decode
-tokens (sequences) per second for the layer.  ``cold_cache`` times the step
-alone with a cache scrub in between; ``gather_read_ceiling`` reads the same
+tokens (sequences) per second for the layer.  Every time is the median of K
+repetitions, each timed alone by HIP events on its stream with a 512 MiB cache
+scrub written before it (``timing`` gives p10 / p90); ``warm_back_to_back``
+is the same step run K times back to back with warm caches, by the host
+clock.  ``gather_read_ceiling`` reads the same
 tiles with no arithmetic (the access pattern's practical ceiling);
 ``stream_read_ceiling`` reads both block pools front to back (HBM's
 streaming-read ceiling on this GPU).
@@ -210,44 +213,53 @@ def main():
 
     P = w.n_parts
     h = ctypes.c_void_p(stream.cuda_stream)
+    from paper_2510_13223_amd import bana
 
-    # Timed region 1: exactly K steps back to back, synchronised on both sides.
-    step_start = torch.cuda.Event(enable_timing=True)
-    step_end = torch.cuda.Event(enable_timing=True)
+    # Every timed figure below is taken the same way: HIP events recorded on the stream the work
+    # runs on, around each repetition alone, with a 512 MiB scrub write between repetitions
+    # (outside the events) so neither L2 nor the 256 MB last-level cache holds K/V from the
+    # previous one; the figure is the median over the K repetitions, with p10 / p90 beside it.
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+
+    def timed_cold(fn, inner=None):
+        """Event-timed repetitions of fn with a scrub before each; returns us per repetition
+        (and, when ``inner`` is given, the us between the two events fn passes to ``inner``)."""
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        with torch.cuda.stream(stream):
+            for k in range(args.steps):
+                scrub.fill_(k & 0xFF)
+                ev[k][0].record(stream)
+                fn()
+                ev[k][1].record(stream)
+        stream.synchronize()
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) * 1e3 for a, b in ev])
+
+    def stats(us):
+        return {"median_us": round(float(np.median(us)), 2), "p10_us": round(float(np.percentile(us, 10)), 2),
+                "p90_us": round(float(np.percentile(us, 90)), 2), "mean_us": round(float(np.mean(us)), 2)}
+
+    # Timed region 1 (the headline): exactly K steps, each timed alone by events after a cache scrub,
+    # synchronised on both sides of the region.
+    step_us = timed_cold(lambda: dw.step_on(h))
+    t_step = float(np.median(step_us)) / 1e6
+    print(f"[bench] timed {args.steps} steps (cold caches): median {t_step * 1e6:.1f} us/step", file=sys.stderr,
+          flush=True)
+
+    # Side figure: the same K steps back to back with warm caches, host clock synchronised on both sides.
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    step_start.record(stream)
     for _ in range(args.steps):
         dw.step_on(h)
-    step_end.record(stream)
     stream.synchronize()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    gpu_ms = step_start.elapsed_time(step_end)
-    ms_per_step = wall * 1e3 / args.steps  # host wall clock, synchronised on both sides
-    print(f"[bench] timed {args.steps} steps: {ms_per_step * 1e3:.1f} us/step", file=sys.stderr, flush=True)
-
-    # Cold caches: the same step K times with events around each step alone and a 512 MiB
-    # scrub write between steps (outside the events), so neither L2 nor the last-level cache
-    # holds K/V from the previous step.
-    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-    cold_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    with torch.cuda.stream(stream):
-        for k in range(args.steps):
-            scrub.fill_(k & 0xFF)
-            cold_ev[k][0].record(stream)
-            dw.step_on(h)
-            cold_ev[k][1].record(stream)
-    stream.synchronize()
-    cold_us = np.array([a.elapsed_time(b) * 1e3 for a, b in cold_ev])
-    del scrub
+    warm_ms = (time.perf_counter() - wall0) * 1e3 / args.steps
+    print(f"[bench] back to back: {warm_ms * 1e3:.1f} us/step", file=sys.stderr, flush=True)
 
     # Practical ceiling of the access pattern: the same K/V tiles read through the same
     # table walk with no arithmetic (bana_debug_gather_read over all partitions).
-    from paper_2510_13223_amd import bana
-
     sink = torch.empty((w.batch, w.num_kv_heads), dtype=torch.int32, device=dev)
 
     def gather():
@@ -256,12 +268,7 @@ def main():
 
     for _ in range(args.warmup):
         gather()
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    for _ in range(args.steps):
-        gather()
-    torch.cuda.synchronize()
-    gather_s = (time.perf_counter() - wall0) / args.steps
+    gather_s = float(np.median(timed_cold(gather))) / 1e6
     print(f"[bench] gather-read ceiling: {gather_s * 1e6:.1f} us", file=sys.stderr, flush=True)
 
     # Streaming ceiling of HBM reads: both pools read front to back (bana_debug_stream_read,
@@ -275,52 +282,44 @@ def main():
 
     for _ in range(args.warmup):
         stream_read()
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    for _ in range(args.steps):
-        stream_read()
-    torch.cuda.synchronize()
-    stream_s = (time.perf_counter() - wall0) / args.steps
+    stream_s = float(np.median(timed_cold(stream_read))) / 1e6
     print(f"[bench] stream-read ceiling: {stream_s * 1e6:.1f} us for {pool_bytes} B", file=sys.stderr, flush=True)
 
-    # Timed region 2: the same K steps with HIP events recorded on the stream the kernel runs on:
-    # (a) one pair around each step's partial-attention launches (back to back, the merge after
-    # the second event), which gives the kernel's mean launch duration for the roofline; (b) one
-    # pair around every single launch, for the split by partition (those records add a little
-    # time per launch).  The step time above is taken without any events.
+    # Timed region 2: the same K steps, scrubbed, with HIP events on the kernel's stream (a) around
+    # each step's back-to-back partial-attention launches (the merge after the second event): the
+    # kernel's mean launch duration for the roofline; (b) around every single launch, for the split
+    # by partition (those records add a little time per launch).
     ev_all = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for k in range(args.steps):
-        ev_all[k][0].record(stream)
-        for p in range(P):
-            dw.partial(p, h)
-        ev_all[k][1].record(stream)
-        dw.merge(h)
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(P)]
           for _ in range(args.steps)]
-    for k in range(args.steps):
-        for p in range(P):
-            ev[k][p][0].record(stream)
-            dw.partial(p, h)
-            ev[k][p][1].record(stream)
-        dw.merge(h)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        for k in range(args.steps):
+            scrub.fill_(k & 0xFF)
+            ev_all[k][0].record(stream)
+            for p in range(P):
+                dw.partial(p, h)
+            ev_all[k][1].record(stream)
+            dw.merge(h)
+        for k in range(args.steps):
+            scrub.fill_(k & 0xFF)
+            for p in range(P):
+                ev[k][p][0].record(stream)
+                dw.partial(p, h)
+                ev[k][p][1].record(stream)
+            dw.merge(h)
     stream.synchronize()
     torch.cuda.synchronize()
 
     # Timed region 3: the same step through the fused entry point (every partition and the
-    # merge in one launch), K times, synchronised on both sides.
+    # merge in one launch).
     for _ in range(args.warmup):
         dw.fused(h)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    for _ in range(args.steps):
-        dw.fused(h)
-    torch.cuda.synchronize()
-    fused_ms = (time.perf_counter() - wall0) * 1e3 / args.steps
+    fused_us = timed_cold(lambda: dw.fused(h))
+    fused_ms = float(np.median(fused_us)) / 1e3
     print(f"[bench] fused path: {fused_ms * 1e3:.1f} us/step", file=sys.stderr, flush=True)
 
     # Timed region 4: KV-block migration of the last (migrated) partition into a second pool.
-
     mig = workloads.make_migration(w, P - 1, seed=1)
     mig_blocks = int(np.sum(mig.blk_end - mig.blk_begin))
     d_k = torch.from_numpy(mig.dst_k.view(np.int16)).view(torch.bfloat16).to(dev)
@@ -336,18 +335,13 @@ def main():
 
     for _ in range(args.warmup):
         migrate()
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    for _ in range(args.steps):
-        migrate()
-    torch.cuda.synchronize()
-    mig_ms = (time.perf_counter() - wall0) * 1e3 / args.steps
+    mig_ms = float(np.median(timed_cold(migrate))) / 1e3
     mig_bytes = mig_blocks * w.num_kv_heads * 8192  # K + V tiles of every migrated block, read once and written once
     del d_k, d_v
     print(f"[bench] migration: {mig_ms * 1e3:.1f} us for {mig_bytes / 1e6:.1f} MB", file=sys.stderr, flush=True)
 
     # Timed region 5: the head split (the cache split along kv heads instead of tokens): each half of
-    # the kv heads over whole sequences, one bana_decode_attn_heads call each, timed by events.
+    # the kv heads over whole sequences, one bana_decode_attn_heads call each.
     hs_begin = torch.zeros(w.batch, dtype=torch.int32, device=dev)
     hs_end = dw.seq_lens
     lens_all = w.seq_lens.astype(np.int64)
@@ -370,21 +364,13 @@ def main():
     for _ in range(args.warmup):
         for i in range(len(hs_ranges)):
             head_call(i)
-    torch.cuda.synchronize()
-    hs_ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in hs_ranges]
-             for _ in range(args.steps)]
-    for row in hs_ev:
-        for i, (a, b) in enumerate(row):
-            a.record(stream)
-            head_call(i)
-            b.record(stream)
-    torch.cuda.synchronize()
-    hs_us = [float(np.mean([row[i][0].elapsed_time(row[i][1]) for row in hs_ev])) * 1e3 for i in range(len(hs_ranges))]
+    hs_us = [float(np.median(timed_cold(lambda i=i: head_call(i)))) for i in range(len(hs_ranges))]
     hs_bytes = [int(lens_all.sum()) * (g1 - g0) * 128 * 2 * 2 for g0, g1 in hs_ranges]
     print(f"[bench] head split: {[round(x, 1) for x in hs_us]} us", file=sys.stderr, flush=True)
+    del scrub
 
     kv_bytes = w.kv_bytes()
-    t_step = ms_per_step / 1e3
+    ms_per_step = t_step * 1e3
     # Partial-attention kernel: algorithmic bytes over its own launch durations.
     alg = [_partial_algorithmic_bytes(w, p) for p in range(P)]
     dur_ms = np.array([[ev[k][p][0].elapsed_time(ev[k][p][1]) for p in range(P)] for k in range(args.steps)])
@@ -394,8 +380,6 @@ def main():
     achieved = mean_bytes / mean_dur_s / 1e9
     partial_kv_gbs = float(np.sum([a[1] for a in alg])) / (float(step_partials_ms.mean()) / 1e3) / 1e9
 
-    # One kernel per partial call when no partition's plan needs workspace; otherwise the call is the
-    # attention kernel plus its chunk (or piece) merge, and the events time both.
     single = all(bana.bana_decode_attn_workspace_bytes(d) == 0 for d in dw.dims)
     roofline_kernel = ("partial_attn_kernel" if single else
                        "bana_decode_attn_partial call (attention kernel + chunk or piece merge)")
@@ -407,34 +391,37 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
-        "gpu_event_ms_per_step": round(gpu_ms / args.steps, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
         "config": _workload_desc(w),
+        "timing": {
+            "method": "HIP events around each step alone on its stream, 512 MiB scrub write between steps "
+                      "(outside the events); value and ms_per_step from the median",
+            **stats(step_us),
+        },
         "frac_of_hbm_peak": round(kv_bytes / t_step / 1e9 / HBM_PEAK_GBS, 4),
         "tokens_per_s": round(w.batch / t_step, 1),
         "tokens_per_s_32_layers": round(w.batch / (32 * t_step), 1),
         "kv_bytes_per_step": kv_bytes,
+        "warm_back_to_back": {
+            "method": "K steps back to back with warm caches, host clock synchronised on both sides",
+            "ms_per_step": round(warm_ms, 5),
+            "value": round(kv_bytes / (warm_ms / 1e3) / 1e9, 2),
+            "unit": "GB/s",
+        },
         "fused_path": {
             "entry_point": "bana_decode_attn_fused",
             "ms_per_step": round(fused_ms, 5),
+            **stats(fused_us),
             "value": round(kv_bytes / (fused_ms / 1e3) / 1e9, 2),
             "unit": "GB/s",
             "frac_of_hbm_peak": round(kv_bytes / (fused_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
             "tokens_per_s": round(w.batch / (fused_ms / 1e3), 1),
         },
         "partial_kernels_kv_gbs": round(partial_kv_gbs, 2),
-        "cold_cache": {
-            "method": "events around each step alone, 512 MiB scrub write between steps",
-            "median_us": round(float(np.median(cold_us)), 2),
-            "p10_us": round(float(np.percentile(cold_us, 10)), 2),
-            "p90_us": round(float(np.percentile(cold_us, 90)), 2),
-            "value": round(kv_bytes / (float(np.median(cold_us)) / 1e6) / 1e9, 2),
-            "unit": "GB/s",
-        },
         "gather_read_ceiling": {
             "entry_point": "bana_debug_gather_read",
             "what": "the step's K/V tiles read through the block table with the attention kernel's load shapes, "
@@ -489,7 +476,7 @@ def main():
             "mean_launch_us": round(mean_dur_s * 1e6, 2),
             "launch_us_per_partition": [round(float(x) * 1e3, 2) for x in dur_ms.mean(axis=0)],
             "launch_timing": "mean launch = HIP events around each step's back-to-back partial launches / "
-                             "partitions; per-partition split from events around every launch",
+                             "partitions (scrubbed steps); per-partition split from events around every launch",
         },
     }
     if args.copy_calibration:

@@ -32,6 +32,10 @@ MUTANTS = [
     ("merge reads empty parts", "      if (v == -INFINITY) continue;\n      double w = exp(v - M);", "      double w = exp(v - M);"),
     ("merge weights unnormalised", "for (int d = 0; d < D; ++d) o[d] /= wsum;", ""),
     ("empty partition lse zero", "        lse[(int64_t)i * Hq + h] = -INFINITY;\n        continue;", "        lse[(int64_t)i * Hq + h] = 0.0;\n        continue;"),
+    ("address export: head-major tile index", "*r = blk < 0 ? -2 : (blk * Hkv + g) * bs + t % bs;",
+     "*r = blk < 0 ? -2 : (g * num_blocks + blk) * bs + t % bs;"),
+    ("address export: reversed slot", "*r = blk < 0 ? -2 : (blk * Hkv + g) * bs + t % bs;",
+     "*r = blk < 0 ? -2 : (blk * Hkv + g) * bs + (bs - 1 - t % bs);"),
 ]
 
 
