@@ -17,7 +17,9 @@
  *  - All tensor arguments are DEVICE pointers owned by the caller, resident
  *    on the current HIP device, 16-byte aligned and densely packed in the
  *    layouts stated below.  The library allocates no memory and keeps no
- *    per-call state; calls are thread-safe.
+ *    per-call state; calls are thread-safe.  (One exception, for callers that
+ *    cannot allocate: bana_decode_attn_partial_noalloc keeps its partials in a
+ *    static device array of the library, shared by its calls on a device.)
  *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
  *    stream).  Nothing synchronises.
  *  - Host-checkable argument errors return before any HIP call:
@@ -131,6 +133,39 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
                                      const int32_t* kv_range_begin, const int32_t* kv_range_end,
                                      float* out_partial, float* lse, void* workspace, size_t workspace_bytes,
                                      void* stream);
+
+/* Bytes of the library's static device scratch (see bana_decode_attn_partial_noalloc). */
+#define BANA_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation:
+ * bana_decode_attn_partial without a caller workspace.  Same arguments (less
+ * the workspace), same results bit for bit and same errors as
+ * bana_decode_attn_partial given a workspace of
+ * bana_decode_attn_workspace_bytes(d) bytes.  Where that call would split
+ * ranges, the partials live in a static device array of the library,
+ * BANA_STATIC_SCRATCH_BYTES (64 MiB) on each device, held from the time the
+ * library's code is loaded on that device until the process ends.  This call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine); its
+ * first call on a device, with that device current, looks the array's device
+ * address up once (hipGetSymbolAddress).
+ *   - Limit: when the launch plan for d needs more workspace than the array
+ *     holds (bana_decode_attn_workspace_bytes(d) > BANA_STATIC_SCRATCH_BYTES),
+ *     the call returns BANA_ERR_UNSUPPORTED before any launch, and
+ *     bana_last_error() names both sizes; use bana_decode_attn_partial with a
+ *     workspace of your own for such dims.
+ *   - Sharing: every call on one device uses the same array and leaves its
+ *     partials there.  Nothing in it needs to start at zero, but calls that
+ *     may overlap on one device (on different streams with no event between
+ *     them, or from several host threads) race for it and give wrong results:
+ *     serialise them, e.g. on one stream.
+ */
+bana_status bana_decode_attn_partial_noalloc(const bana_dims* d, const void* q, const void* k_cache,
+                                             const void* v_cache, const int32_t* block_table,
+                                             const int32_t* seq_lens, const int32_t* kv_range_begin,
+                                             const int32_t* kv_range_end, float* out_partial, float* lse,
+                                             void* stream);
 
 /*
  * Head-split partition: the literal reading of Sec. 4.1(2), where the KV
@@ -269,7 +304,9 @@ bana_status bana_copy_async(void* dst, const void* src, size_t bytes, void* stre
 /* Static text for a status code. */
 const char* bana_status_string(bana_status s);
 
-/* Text of the last HIP error seen by a call on this thread ("" if none). */
+/* Text of the last error a call on this thread described in detail: the HIP
+ * error text of a failed launch, or the sizes behind a refused
+ * bana_decode_attn_partial_noalloc call ("" if none). */
 const char* bana_last_error(void);
 
 /*

@@ -46,9 +46,10 @@ class bana_dims(ctypes.Structure):
 
 
 class BanaError(RuntimeError):
-    def __init__(self, status: int, what: str):
+    def __init__(self, status: int, what: str, detail: str = ""):
         self.status = status
-        detail = lib().bana_last_error().decode() if status == BANA_ERR_DEVICE else ""
+        if not detail and status == BANA_ERR_DEVICE:
+            detail = lib().bana_last_error().decode()
         msg = f"{what}: {lib().bana_status_string(status).decode()} ({status})"
         super().__init__(msg + (f": {detail}" if detail else ""))
 
@@ -68,6 +69,8 @@ def lib() -> ctypes.CDLL:
     D = ctypes.POINTER(bana_dims)
     L.bana_decode_attn_partial.argtypes = [D, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     L.bana_decode_attn_partial.restype = ctypes.c_int
+    L.bana_decode_attn_partial_noalloc.argtypes = [D, P, P, P, P, P, P, P, P, P, P]
+    L.bana_decode_attn_partial_noalloc.restype = ctypes.c_int
     L.bana_decode_attn_workspace_bytes.argtypes = [D]
     L.bana_decode_attn_workspace_bytes.restype = ctypes.c_size_t
     L.bana_decode_attn_fused.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_int32, P, P, P, ctypes.c_size_t, P]
@@ -191,6 +194,33 @@ def bana_decode_attn_partial(q, k_cache, v_cache, block_table, seq_lens, kv_rang
         _stream(stream))
     if st != BANA_OK:
         raise BanaError(st, "bana_decode_attn_partial")
+
+
+STATIC_SCRATCH_BYTES = 64 << 20  # BANA_STATIC_SCRATCH_BYTES
+
+
+def bana_decode_attn_partial_noalloc(q, k_cache, v_cache, block_table, seq_lens, kv_range_begin, kv_range_end,
+                                     out_partial, lse, stream=None, dims: Optional[bana_dims] = None,
+                                     max_range_tokens: int = 0) -> None:
+    """``bana_decode_attn_partial`` with the library's static device scratch in place of a workspace
+    (for callers that cannot allocate); see ``bana_decode_attn_partial_noalloc`` in include/bana.h.
+    Calls that may overlap on one device share that scratch and must be serialised."""
+    B, Hq, D = _check_attn_inputs(q, k_cache, v_cache, block_table, seq_lens)
+    _need(kv_range_begin, "kv_range_begin", torch.int32, (B,))
+    _need(kv_range_end, "kv_range_end", torch.int32, (B,))
+    _need(out_partial, "out_partial", torch.float32, (B, Hq, D))
+    _need(lse, "lse", torch.float32, (B, Hq))
+    _same_device(q, kv_range_begin, kv_range_end, out_partial, lse)
+    if dims is None:
+        dims = dims_for(q, k_cache, block_table, max_range_tokens)
+    _check_dims(dims, q, k_cache, block_table)
+    st = lib().bana_decode_attn_partial_noalloc(
+        ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens),
+        _ptr(kv_range_begin), _ptr(kv_range_end), _ptr(out_partial), _ptr(lse), _stream(stream))
+    if st != BANA_OK:
+        text = lib().bana_last_error().decode()
+        raise BanaError(st, "bana_decode_attn_partial_noalloc",
+                        text if text.startswith("bana_decode_attn_partial_noalloc:") else "")
 
 
 def _check_attn_inputs(q, k_cache, v_cache, block_table, seq_lens):

@@ -22,6 +22,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libbana.so")
 SOURCES = ["attn_partial.hip", "merge.hip", "migrate.hip", "validate.hip", "debug_rows.hip", "gather_read.hip",
+           "scratch.hip",
            "bana_api.cpp"]
 
 ARCH = "gfx950"

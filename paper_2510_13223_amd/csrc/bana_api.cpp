@@ -298,6 +298,21 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
   return device_status(bana::launch_merge(ws_out, ws_lse, plan.nc, m, out, lse, s));
 }
 
+bana_status check_partial_args(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
+                               const int32_t* block_table, const int32_t* seq_lens, const int32_t* kv_range_begin,
+                               const int32_t* kv_range_end, const float* out_partial, const float* lse,
+                               const void* workspace) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !kv_range_begin || !kv_range_end || !out_partial ||
+      !lse)
+    return BANA_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out_partial) ||
+      (workspace != nullptr && !aligned16(workspace)))
+    return BANA_ERR_INVALID;
+  return BANA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -307,16 +322,37 @@ bana_status bana_decode_attn_partial(const bana_dims* d, const void* q, const vo
                                      const int32_t* kv_range_begin, const int32_t* kv_range_end,
                                      float* out_partial, float* lse, void* workspace, size_t workspace_bytes,
                                      void* stream) {
-  const bana_status st = check_dims(d);
+  const bana_status st = check_partial_args(d, q, k_cache, v_cache, block_table, seq_lens, kv_range_begin,
+                                            kv_range_end, out_partial, lse, workspace);
   if (st != BANA_OK) return st;
-  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !kv_range_begin || !kv_range_end || !out_partial ||
-      !lse)
-    return BANA_ERR_INVALID;
-  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out_partial) ||
-      (workspace != nullptr && !aligned16(workspace)))
-    return BANA_ERR_INVALID;
   return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, 1, 0, d->num_kv_heads,
                        out_partial, lse, workspace, workspace_bytes, stream);
+}
+
+bana_status bana_decode_attn_partial_noalloc(const bana_dims* d, const void* q, const void* k_cache,
+                                             const void* v_cache, const int32_t* block_table,
+                                             const int32_t* seq_lens, const int32_t* kv_range_begin,
+                                             const int32_t* kv_range_end, float* out_partial, float* lse,
+                                             void* stream) {
+  const bana_status st = check_partial_args(d, q, k_cache, v_cache, block_table, seq_lens, kv_range_begin,
+                                            kv_range_end, out_partial, lse, nullptr);
+  if (st != BANA_OK) return st;
+  // The plan and the workspace it needs are those of bana_decode_attn_partial with a
+  // workspace of bana_decode_attn_workspace_bytes(d) bytes; a plan the static scratch
+  // cannot hold is refused rather than run differently.
+  const size_t need = workspace_for(d, make_plan(d));
+  if (need > bana::kStaticScratchBytes) {
+    g_last_error = "bana_decode_attn_partial_noalloc: the launch plan for these dims needs " + std::to_string(need) +
+                   " bytes of scratch, the library's static scratch holds " +
+                   std::to_string(bana::kStaticScratchBytes) +
+                   " (call bana_decode_attn_partial with a workspace of that size instead)";
+    return BANA_ERR_UNSUPPORTED;
+  }
+  void* scratch = nullptr;
+  const hipError_t e = bana::static_scratch(&scratch);
+  if (e != hipSuccess) return device_status(e);
+  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, 1, 0, d->num_kv_heads,
+                       out_partial, lse, scratch, bana::kStaticScratchBytes, stream);
 }
 
 bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,

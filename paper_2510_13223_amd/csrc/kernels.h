@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "bana.h"
+
 namespace bana {
 
 struct PartialArgs {
@@ -81,6 +83,11 @@ hipError_t launch_gather_read(const void* k, const void* v, const int32_t* table
 // Sequential read of `bytes` (a multiple of 16) by n_groups workgroups of 256 threads;
 // sink[w] = XOR of the 32-bit words workgroup w read.
 hipError_t launch_stream_read(const void* src, size_t bytes, int n_groups, uint32_t* sink, hipStream_t stream);
+
+// The library's static device scratch (bana_decode_attn_partial_noalloc): its size, and its
+// address on the current device (looked up once per device, then cached).
+constexpr size_t kStaticScratchBytes = BANA_STATIC_SCRATCH_BYTES;
+hipError_t static_scratch(void** ptr);
 
 // Address export for the tests (rows of the K pool visited per logical token).
 hipError_t launch_debug_rows(const int32_t* table, const int32_t* begin, const int32_t* end, int B, int Hkv,

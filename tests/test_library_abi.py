@@ -291,3 +291,33 @@ def test_plain_c_caller_builds_against_the_header(lib):
         oracle.build()
     path = _c_build_module().build()
     assert os.access(path, os.X_OK)
+
+
+def test_noalloc_checks_arguments_and_refuses_plans_beyond_the_static_scratch(lib):
+    def noalloc(dd, ptrs=None):
+        p = ptrs or [FAKE] * 9
+        return lib.bana_decode_attn_partial_noalloc(ctypes.byref(dd) if dd is not None else None, *p, None)
+
+    assert noalloc(None) == -1
+    assert noalloc(_dims(head_dim=64)) == -2
+    for i in range(9):
+        ptrs = [FAKE] * 9
+        ptrs[i] = None
+        assert noalloc(_dims(), ptrs) == -1, i
+    ptrs = [FAKE] * 9
+    ptrs[0] = ctypes.c_void_p(0x100008)
+    assert noalloc(_dims(), ptrs) == -1
+    # 256 chunk partials of 64 x 32 rows need far more than the static scratch: refused before any HIP call.
+    d = _dims(batch=64, num_q_heads=32, num_kv_heads=8, chunks_hint=256, waves_hint=1)
+    need = lib.bana_decode_attn_workspace_bytes(ctypes.byref(d))
+    assert need > bana.STATIC_SCRATCH_BYTES
+    assert noalloc(d) == -2
+    msg = lib.bana_last_error().decode()
+    assert msg.startswith("bana_decode_attn_partial_noalloc:")
+    assert str(need) in msg and str(bana.STATIC_SCRATCH_BYTES) in msg
+
+
+def test_static_scratch_size_matches_the_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define BANA_STATIC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == bana.STATIC_SCRATCH_BYTES
