@@ -95,7 +95,7 @@ typedef struct {
   int32_t chunks_hint;        /* chunks a range may be split into (needs workspace) */
   int32_t plan_hint;          /* 0 = choose; 1 = chunked launch; 2 = balanced launch
                                  (equal block intervals per wavefront across
-                                 sequences; needs workspace, batch <= 64 and
+                                 sequences; needs workspace, batch <= 2048 and
                                  batch * 64 * max_blocks_per_seq <= 2^31 - 1,
                                  otherwise the chunked launch runs) */
   int64_t total_range_tokens; /* sum over sequences of kv_range_end - kv_range_begin */
@@ -104,6 +104,10 @@ typedef struct {
    * short ones fill the end of the launch).  NULL = natural order.  Results
    * do not depend on it. */
   const int32_t* seq_order;
+  /* Sequences whose range (all ranges, for the fused call) covers at least
+   * one token; with total_range_tokens it gives the mean range of the
+   * sequences that have work.  0 = unknown (taken as batch). */
+  int32_t nonempty_ranges;
 } bana_dims;
 
 /*

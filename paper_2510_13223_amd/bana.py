@@ -42,6 +42,7 @@ class bana_dims(ctypes.Structure):
         ("plan_hint", ctypes.c_int32),
         ("total_range_tokens", ctypes.c_int64),
         ("seq_order", ctypes.c_void_p),
+        ("nonempty_ranges", ctypes.c_int32),
     ]
 
 
@@ -103,14 +104,15 @@ def lib() -> ctypes.CDLL:
 def make_dims(batch: int, num_q_heads: int, num_kv_heads: int, max_blocks_per_seq: int, num_blocks: int,
               max_range_tokens: int = 0, waves_hint: int = 0, chunks_hint: int = 0,
               total_range_tokens: int = 0, seq_order: Optional[torch.Tensor] = None,
-              plan_hint: int = 0) -> bana_dims:
+              plan_hint: int = 0, nonempty_ranges: int = 0) -> bana_dims:
     """Dims for a call; ``seq_order`` (device int32 [batch], kept alive by the caller) is a dispatch hint,
-    ``plan_hint`` 0 / 1 / 2 = library's choice / chunked launch / balanced launch."""
+    ``plan_hint`` 0 / 1 / 2 = library's choice / chunked launch / balanced launch, ``nonempty_ranges``
+    the number of sequences with a non-empty range (0 = unknown)."""
     if seq_order is not None:
         _need(seq_order, "seq_order", torch.int32, (batch,))
     return bana_dims(batch, num_q_heads, num_kv_heads, HEAD_DIM, BLOCK_SIZE, max_blocks_per_seq, num_blocks,
                      max_range_tokens, waves_hint, chunks_hint, plan_hint, total_range_tokens,
-                     None if seq_order is None else seq_order.data_ptr())
+                     None if seq_order is None else seq_order.data_ptr(), nonempty_ranges)
 
 
 def _ptr(t: Optional[torch.Tensor]):

@@ -21,7 +21,7 @@
 //    longer than one chunk leaves one partial per chunk in caller workspace,
 //    merged by the merge kernel with the same log-sum-exp algebra as the
 //    partition merge.
-//  * balanced (uneven ranges of few sequences): the virtual blocks of all
+//  * balanced (uneven ranges, up to 2048 sequences): the virtual blocks of all
 //    sequences, in sequence order, form one list per kv head, cut into K
 //    equal intervals of S = ceil(U / K) blocks (U = blocks of the whole call),
 //    one per wavefront.  A wavefront walks its interval block by block,
@@ -399,53 +399,90 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   }
 }
 
-// Balanced launch (batch <= 64): wavefront k of kv head g walks the blocks
-// [k S, (k + 1) S) (clipped to U) of the call's virtual block list and leaves
-// one partial per sequence piece in slot k + b of the piece buffers
-// ([slot][out_hq][128] and [slot][out_hq]).  Every wavefront computes the schedule
-// itself, one sequence per lane: block counts N_b, their prefix sums by lane
-// shuffles, U and S; the sequence holding block pos is the number of
-// sequences whose blocks end at or before pos.  The first wavefront of the
-// call also stores the prefix sums (prefix[0..B]) for the merge.
+// Balanced launch: wavefront k of kv head g walks the blocks [k S, (k + 1) S)
+// (clipped to U) of the call's virtual block list -- every sequence's blocks
+// over all its ranges, in sequence order -- and leaves one partial per
+// sequence piece in slot k + b of the piece buffers ([slot][out_hq][128] and
+// [slot][out_hq]).  The schedule is computed by each workgroup in LDS: the
+// block count N_b of every sequence, their inclusive prefix sums P_b by a
+// workgroup-wide scan, U = P_{B-1} and S = ceil(U / K); the sequence holding
+// block pos is the first b with P_b > pos (binary search).  The first
+// workgroup also stores the prefix sums (prefix[0..B], exclusive) for the
+// piece merge.
 template <int W>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) void balanced_attn_kernel(
     PartialArgs a, int32_t* __restrict__ prefix, int K) {
+  constexpr int kThreads = 64 * W;
+  constexpr int kPerThread = (kMaxBalancedBatch + kThreads - 1) / kThreads;
+  __shared__ int32_t sm_incl[kMaxBalancedBatch];
+  __shared__ int32_t sm_wave_sum[W];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15;
   const int quad = lane >> 4;
-  const int g = a.g0 + (int)(blockIdx.x % (unsigned)a.ng);
-  const int k = (int)(blockIdx.x / (unsigned)a.ng) * W + wave;
-  if (k >= K) return;
-  const int G = a.G;
-  const int hq0 = g * G;
+  const int B = a.B;
 
-  int n_lane = 0;  // blocks of sequence `lane` over all its ranges
-  if (lane < a.B) {
-    for (int p = 0; p < a.n_parts; ++p) {
-      const int t0 = a.begin[(int64_t)p * a.B + lane];
-      const int t1 = a.end[(int64_t)p * a.B + lane];
-      if (t1 > t0) n_lane += ((t1 - 1) >> 4) - (t0 >> 4) + 1;
+  // Thread t counts the blocks of sequences [t * per, t * per + per) (per <= kPerThread).
+  const int per = (B + kThreads - 1) / kThreads;
+  const int s0 = threadIdx.x * per;
+  int cnt[kPerThread];
+  int local = 0;
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    cnt[i] = 0;
+    const int b = s0 + i;
+    if (i < per && b < B) {
+      for (int p = 0; p < a.n_parts; ++p) {
+        const int t0 = a.begin[(int64_t)p * B + b];
+        const int t1 = a.end[(int64_t)p * B + b];
+        if (t1 > t0) cnt[i] += ((t1 - 1) >> 4) - (t0 >> 4) + 1;
+      }
     }
+    local += cnt[i];
   }
-  int incl = n_lane;  // blocks of sequences 0..lane
+  // Workgroup-wide exclusive scan of the per-thread totals: within the wave by shuffles, then
+  // across the W waves through LDS.
+  int incl = local;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
     const int y = __shfl_up(incl, off);
     if (lane >= off) incl += y;
   }
-  if (k == 0 && g == a.g0) {
-    if (lane < a.B) prefix[lane + 1] = incl;
-    if (lane == 0) prefix[0] = 0;
+  if (lane == 63) sm_wave_sum[wave] = incl;
+  __syncthreads();
+  int before = incl - local;
+  for (int w = 0; w < wave; ++w) before += sm_wave_sum[w];
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    const int b = s0 + i;
+    before += cnt[i];
+    if (i < per && b < B) sm_incl[b] = before;
   }
-  const int U = __builtin_amdgcn_readlane(incl, a.B - 1);
+  __syncthreads();
+
+  if (blockIdx.x == 0) {
+    for (int i = threadIdx.x; i <= B; i += kThreads) prefix[i] = i == 0 ? 0 : sm_incl[i - 1];
+  }
+  const int g = a.g0 + (int)(blockIdx.x % (unsigned)a.ng);
+  const int k = (int)(blockIdx.x / (unsigned)a.ng) * W + wave;
+  if (k >= K) return;
+  const int G = a.G;
+  const int hq0 = g * G;
+  const int U = sm_incl[B - 1];
   const int64_t S = U > K ? ((int64_t)U + K - 1) / K : 1;
   const int u1 = (int)min((int64_t)U, (k + 1) * S);
   int pos = (int)min((int64_t)U, k * S);
 
   while (pos < u1) {
-    const int b = __builtin_popcountll(__ballot(lane < a.B && incl <= pos));  // sequence holding block pos
-    const int pb = b > 0 ? __builtin_amdgcn_readlane(incl, b - 1) : 0;
+    // Sequence holding block pos: the first b with P_b > pos (wave-uniform binary search).
+    int lo = 0, hi = B - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (sm_incl[mid] > pos) hi = mid;
+      else lo = mid + 1;
+    }
+    const int b = __builtin_amdgcn_readfirstlane(lo);
+    const int pb = b > 0 ? sm_incl[b - 1] : 0;
     Segments sg;
     sg.load(a, b, lane, a.n_parts);
     const int nb = sg.total(a.n_parts);
@@ -492,6 +529,7 @@ hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stre
 }
 
 hipError_t launch_balanced_attn(const PartialArgs& a, int32_t* prefix, int K, hipStream_t stream) {
+  if (a.B < 1 || a.B > kMaxBalancedBatch || K < 1) return hipErrorInvalidValue;  // the LDS schedule's bounds
   const unsigned nwg = (unsigned)((K + kBalancedWaves - 1) / kBalancedWaves) * (unsigned)a.ng;
   hipLaunchKernelGGL(balanced_attn_kernel<kBalancedWaves>, dim3(nwg), dim3(64 * kBalancedWaves), 0, stream, a,
                      prefix, K);

@@ -22,6 +22,10 @@ constexpr int kHeadDim = 128;
 constexpr int kBlockSize = 16;
 constexpr int kMaxGroup = 16;           // query heads per kv head handled by one MFMA column tile
 constexpr int kTargetWaves = 256 * 16;  // 256 CUs x 16 resident wavefronts: one full dispatch round
+// Wavefronts of a balanced launch: 8 per CU, each walking twice the blocks it would in a full round.
+// Measured on MI355X (long and mixed workloads, cold caches): 2048 wavefronts beat 4096 (each
+// wavefront's start-up is paid over more blocks) and 1024 (too few blocks in flight).
+constexpr int kBalancedTargetWaves = 256 * 8;
 constexpr int kMinBlocksPerWave = 8;    // below this a wavefront spends more time starting than streaming
 constexpr int kMaxBlocksPerWave = 64;   // longest run of blocks one wavefront should walk (no hints)
 constexpr int kMaxChunks = 256;
@@ -38,7 +42,7 @@ bana_status check_dims(const bana_dims* d) {
     return BANA_ERR_INVALID;
   if (d->num_q_heads % d->num_kv_heads != 0) return BANA_ERR_INVALID;
   if (d->max_range_tokens < 0 || d->chunks_hint < 0 || d->plan_hint < 0 || d->plan_hint > 2 ||
-      d->total_range_tokens < 0)
+      d->total_range_tokens < 0 || d->nonempty_ranges < 0)
     return BANA_ERR_INVALID;
   if (d->waves_hint != 0 && d->waves_hint != 1 && d->waves_hint != 2 && d->waves_hint != 4 && d->waves_hint != 8)
     return BANA_ERR_INVALID;
@@ -60,57 +64,75 @@ struct Plan {
   int cmin;       // minimum blocks per chunk
   bool balanced;  // equal block intervals per wavefront across sequences
   int K;          // balanced: wavefronts per kv head
+  int kp;         // balanced: thread groups per row of the piece merge
 };
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 // Workgroups are (chunk, sequence, kv head) with `waves` wavefronts each.
 // Aim for one full round of resident wavefronts (256 CUs x 16).  With the
-// range hints (longest range, total tokens):
-//  - uneven ranges (longest > 1.25 x mean) get 8 waves per workgroup, so the
-//    long ranges finish early while short ones fill the rest of the GPU;
-//  - when the (sequence, kv head) pairs alone cannot fill the round, every
-//    range is cut into chunks of one wavefront's even share of the call's
-//    blocks, enlarged so the rounding of each range to whole chunks still
-//    fits one round (a second, partly filled round would double the time of
-//    its workgroups);
+// range hints (longest range, total tokens, sequences with a non-empty
+// range -- the "active" ones; the others cost a workgroup that exits at once):
+//  - uneven ranges (longest > 1.25 x the mean over active sequences) get 8
+//    waves per workgroup, so the long ranges finish early while short ones
+//    fill the rest of the GPU;
+//  - when the active (sequence, kv head) pairs alone cannot fill the round,
+//    every range is cut into chunks of one wavefront's even share of the
+//    call's blocks, enlarged so the rounding of each range to whole chunks
+//    still fits one round (a second, partly filled round would double the
+//    time of its workgroups);
 //  - otherwise a range is only cut when its workgroup would take more than
 //    twice the even share, into chunks of twice the even share.
 // Chunks need workspace; without it the call runs unsplit.  Without hints
 // the table width bounds the range length.
 //
-// Balanced launch (batch <= 64): one round of wavefronts per kv head, each
-// over an equal interval of the call's blocks in sequence order, the pieces
-// of a sequence merged afterwards.  Chosen when the longest hinted range
-// exceeds 1.5 x the mean, the (sequence, kv head) pairs cannot fill one round
-// and the call has at least kMinBlocksPerWave blocks per wavefront (or asked
-// for by plan_hint 2): that is where the chunked plan has to round every
-// range to whole chunks within a single round.  With a milder spread that
-// rounding costs less than the piece merge, and with many pairs several
-// dispatch rounds, longest range first, balance by themselves.
+// Balanced launch (batch <= kMaxBalancedBatch): kBalancedTargetWaves
+// wavefronts split over the kv heads, each over an equal interval of the
+// call's blocks in sequence order, the pieces of a sequence merged
+// afterwards.  Chosen when the ranges are uneven (longest > 1.25 x the mean),
+// the active (sequence, kv head) pairs number at most a quarter of a round's
+// wavefronts and the call has at least kMinBlocksPerWave blocks per
+// wavefront (or asked for by plan_hint 2): there the chunked plan has to
+// round every range to whole chunks within one or two rounds.  With even
+// ranges that rounding costs less than the piece merge, and with many pairs
+// several dispatch rounds, longest range first, balance by themselves
+// (measured on MI355X, cold caches: mixed's 2048-pair calls 193 / 251 us
+// chunked against 214 / 263 us balanced; its 1024-pair head halves 317
+// against 278 us; long's fused call, 1.3 x spread, 494 against 478 us).
 Plan make_plan(const bana_dims* d) {
   const int64_t pairs = (int64_t)d->batch * d->num_kv_heads;
+  const int64_t active = d->nonempty_ranges > 0 ? std::min<int64_t>(d->nonempty_ranges, d->batch) : d->batch;
+  const int64_t active_pairs = active * d->num_kv_heads;
   int64_t bound = d->max_blocks_per_seq;  // blocks of the longest range
   if (d->max_range_tokens > 0) bound = std::min<int64_t>(bound, (d->max_range_tokens + kBlockSize - 1) / kBlockSize);
   bound = std::max<int64_t>(bound, 1);
-  int64_t wpp = (kTargetWaves + pairs - 1) / pairs;
+  int64_t wpp = (kTargetWaves + active_pairs - 1) / active_pairs;
   wpp = std::max<int64_t>(1, std::min<int64_t>(wpp, std::max<int64_t>(1, bound / kMinBlocksPerWave)));
   const bool hinted = d->total_range_tokens > 0;
   const int64_t mean_blocks =
-      hinted ? std::max<int64_t>(1, d->total_range_tokens / (kBlockSize * (int64_t)d->batch) + 1) : bound;
+      hinted ? std::max<int64_t>(1, d->total_range_tokens / (kBlockSize * active) + 1) : bound;
   const bool uneven = hinted && 4 * bound > 5 * mean_blocks;
   Plan p;
   p.balanced = false;
-  p.K = std::max(1, kTargetWaves / (bana::kBalancedWaves * d->num_kv_heads)) * bana::kBalancedWaves;
+  p.K = std::max(1, kBalancedTargetWaves / (bana::kBalancedWaves * d->num_kv_heads)) * bana::kBalancedWaves;
+  p.kp = 1;
   // The balanced schedule counts the blocks of all ranges of all sequences in 32 bits.
   const bool fits32 = (int64_t)d->batch * kMaxFusedParts * d->max_blocks_per_seq <= INT32_MAX;
   if (d->batch <= bana::kMaxBalancedBatch && fits32 && d->waves_hint == 0 && d->chunks_hint == 0 &&
       d->plan_hint != 1) {
-    const int64_t call_blocks = hinted ? d->total_range_tokens / kBlockSize + d->batch : 0;
-    const bool few_pairs = pairs < kTargetWaves / bana::kBalancedWaves;
-    const bool very_uneven = hinted && 2 * bound > 3 * mean_blocks;  // longest range > 1.5 x mean
-    p.balanced =
-        d->plan_hint == 2 || (very_uneven && few_pairs && call_blocks >= (int64_t)kMinBlocksPerWave * p.K);
+    const int64_t call_blocks = hinted ? d->total_range_tokens / kBlockSize + active : 0;
+    const bool few_pairs = 4 * active_pairs <= kTargetWaves;
+    p.balanced = d->plan_hint == 2 || (uneven && few_pairs && call_blocks >= (int64_t)kMinBlocksPerWave * p.K);
+  }
+  if (p.balanced) {
+    // Pieces of the row with the most: its blocks over intervals of at least s_lo blocks, plus
+    // the two partly covered intervals at its ends.  Many pieces per row, or few rows (long
+    // sequences of a small batch), spread each row's pieces over several thread groups.
+    const int64_t u_lo = hinted ? std::max<int64_t>(1, d->total_range_tokens / kBlockSize) : 1;
+    const int64_t s_lo = std::max<int64_t>(1, u_lo / p.K);
+    const int64_t pieces = (bound + 1) / s_lo + 2;
+    const int64_t rows = (int64_t)d->batch * d->num_q_heads;
+    p.kp = pieces >= 32 || rows < 4096 ? 8 : pieces >= 16 ? 4 : pieces >= 8 ? 2 : 1;
   }
   if (p.balanced) {
     p.waves = bana::kBalancedWaves;
@@ -134,12 +156,13 @@ Plan make_plan(const bana_dims* d) {
   } else if (hinted) {
     // (block, kv head) units of the call and the blocks per wavefront if they
     // were spread evenly over one round of resident wavefronts.
-    const int64_t units = mean_blocks * pairs;
+    const int64_t units = mean_blocks * active_pairs;
     const int64_t even = (units + kTargetWaves - 1) / kTargetWaves;
     const int64_t slots = kTargetWaves / p.waves;
     int64_t per_wave;
-    if (pairs < slots) {
-      per_wave = std::max<int64_t>(even, (units + p.waves * (slots - pairs) - 1) / (p.waves * (slots - pairs)));
+    if (active_pairs < slots) {
+      per_wave = std::max<int64_t>(
+          even, (units + p.waves * (slots - active_pairs) - 1) / (p.waves * (slots - active_pairs)));
     } else if (bound > 2 * even * p.waves) {
       per_wave = 2 * even;
     } else {
@@ -279,7 +302,7 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
     a.lse = ws_lse;
     hipError_t e = bana::launch_balanced_attn(a, prefix, plan.K, s);
     if (e != hipSuccess) return device_status(e);
-    return device_status(bana::launch_merge_pieces(ws_out, ws_lse, prefix, plan.K, m, out, lse, s));
+    return device_status(bana::launch_merge_pieces(ws_out, ws_lse, prefix, plan.K, plan.kp, m, out, lse, s));
   }
   if (plan.nc == 1) {
     a.out = out;

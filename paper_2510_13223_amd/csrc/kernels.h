@@ -33,8 +33,8 @@ struct PartialArgs {
 // Partial attention: one workgroup of `waves` wavefronts per (chunk, sequence, kv head).
 hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stream);
 
-constexpr int kBalancedWaves = 8;       // wavefronts per workgroup of the balanced launch
-constexpr int kMaxBalancedBatch = 64;  // one sequence per lane of the in-kernel schedule
+constexpr int kBalancedWaves = 8;         // wavefronts per workgroup of the balanced launch
+constexpr int kMaxBalancedBatch = 2048;  // sequences of the in-kernel schedule (prefix sums held in LDS)
 
 // Balanced launch: K wavefronts per kv head, each over an equal interval of the call's virtual
 // blocks; a.out / a.lse are piece buffers [K + B][out_hq][128] / [K + B][out_hq]; prefix [B + 1]
@@ -49,9 +49,10 @@ struct MergeRows {
   int hn, in_hq, in_h0, out_hq, out_h0;
 };
 
-// Merge of the balanced launch's pieces (slots [K + B][in_hq]) into out / lse_out.
-hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, MergeRows m,
-                               float* out, float* lse_out, hipStream_t stream);
+// Merge of the balanced launch's pieces (slots [K + B][in_hq]) into out / lse_out; kp (1, 2, 4 or 8)
+// thread groups per merged row share its pieces.
+hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, int kp,
+                               MergeRows m, float* out, float* lse_out, hipStream_t stream);
 
 // Log-sum-exp merge of n_parts partials ([n_parts][B][in_hq][128] / [n_parts][B][in_hq]) into out / lse_out.
 // Kernel and summation order depend only on n_parts and B x hn.

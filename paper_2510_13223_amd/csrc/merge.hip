@@ -81,7 +81,7 @@ __global__ __launch_bounds__(256) void merge_few_kernel(const float* __restrict_
   if (lse_out != nullptr && d4 == 0) lse_out[orow] = M + logf(wsum);
 }
 
-constexpr int kUnroll = 4;  // partial rows in flight per lane
+constexpr int kUnroll = 4;  // partial rows per round (two rounds in flight per lane)
 
 // Any number of parts.  Group k (of KP) of a row takes parts k, k + KP, ...;
 // its q-th part is p = k + KP q.  Part p of merged row r (head i of sequence
@@ -131,9 +131,17 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
   const float* lrow = lses + (int64_t)k * prow + base;           // lse of the q-th part: lrow[q * lstride]
   const float* orow = outs + ((int64_t)k * prow + base) * 128;  // its row: orow + q * lstride * 128
 
-  // Group max: lane d4 reads parts q = d4, d4 + 32, ...
+  // Group max: lane d4 reads parts q = d4, d4 + 32, ...  The first round of partial rows is
+  // requested at the same time: rows do not depend on any lse (the weights reach them by
+  // shuffle), so the group waits on one round of memory latency for both.  Then the rows stream
+  // in rounds of kUnroll, the next round requested before the current one is summed.  Rows of
+  // empty parts are loaded too (they lie inside the part buffer) but never enter a sum.
   float l0 = -INFINITY;
   if (d4 < nq) l0 = lrow[d4 * lstride];
+  f32x4 o[kUnroll];
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u)
+    if (u < nq) o[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(orow + u * lstride * 128) + d4);
   float m = l0;
   for (int q = d4 + 32; q < nq; q += 32) m = fmaxf(m, lrow[q * lstride]);
 #pragma unroll
@@ -142,29 +150,30 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
   float wsum = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   if (m != -INFINITY) {
-    for (int q0 = 0; q0 < nq; q0 += 32) {
-      // Weight of part q0 + d4 on lane d4 (0 past the end and for empty parts).
-      const float lq = q0 == 0 ? l0 : (q0 + d4 < nq ? lrow[(q0 + d4) * lstride] : -INFINITY);
-      const float wq = lq == -INFINITY ? 0.f : expf(lq - m);
-      const int nr = min(32, nq - q0);  // parts of this round
-      int j = 0;
-      for (; j + kUnroll <= nr; j += kUnroll) {
-        f32x4 o[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-          o[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(orow + (q0 + j + u) * lstride * 128) + d4);
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-          const float w = __shfl(wq, j + u, 32);
-          wsum += w;
-          if (w != 0.f) acc += w * o[u];
-        }
+    // Weight of part 32r + d4 on lane d4 for the current round r of 32 parts (0 past the end
+    // and for empty parts).
+    float wq = l0 == -INFINITY ? 0.f : expf(l0 - m);
+#pragma unroll 1
+    for (int q = 0; q < nq; q += kUnroll) {
+      if (q > 0 && (q & 31) == 0) {
+        const float lq = q + d4 < nq ? lrow[(q + d4) * lstride] : -INFINITY;
+        wq = lq == -INFINITY ? 0.f : expf(lq - m);
       }
-      for (; j < nr; ++j) {
-        const f32x4 o = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(orow + (q0 + j) * lstride * 128) + d4);
-        const float w = __shfl(wq, j, 32);
-        wsum += w;
-        if (w != 0.f) acc += w * o;
+      f32x4 cur[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) cur[u] = o[u];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u)
+        if (q + kUnroll + u < nq)
+          o[u] = __builtin_nontemporal_load(
+              reinterpret_cast<const f32x4*>(orow + (q + kUnroll + u) * lstride * 128) + d4);
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        if (q + u < nq) {
+          const float w = __shfl(wq, (q + u) & 31, 32);
+          wsum += w;
+          if (w != 0.f) acc += w * cur[u];
+        }
       }
     }
   }
@@ -237,13 +246,17 @@ hipError_t launch_merge(const float* outs, const float* lses, int n_parts, Merge
   return launch_many<1>(outs, lses, n_parts, m, out, lse_out, stream);
 }
 
-hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, MergeRows m,
-                               float* out, float* lse_out, hipStream_t stream) {
+hipError_t launch_merge_pieces(const float* outs, const float* lses, const int32_t* prefix, int K, int kp,
+                               MergeRows m, float* out, float* lse_out, hipStream_t stream) {
   const int64_t rows = m.B * m.hn;
   if (rows == 0) return hipSuccess;
-  // Few rows come with long sequences, hence many pieces per row: spread them over 8 thread groups.
-  if (rows < 4096) return launch_many<8, true>(outs, lses, 0, m, out, lse_out, stream, prefix, K);
-  return launch_many<1, true>(outs, lses, 0, m, out, lse_out, stream, prefix, K);
+  switch (kp) {
+    case 1: return launch_many<1, true>(outs, lses, 0, m, out, lse_out, stream, prefix, K);
+    case 2: return launch_many<2, true>(outs, lses, 0, m, out, lse_out, stream, prefix, K);
+    case 4: return launch_many<4, true>(outs, lses, 0, m, out, lse_out, stream, prefix, K);
+    case 8: return launch_many<8, true>(outs, lses, 0, m, out, lse_out, stream, prefix, K);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace bana

@@ -62,7 +62,8 @@ class DeviceWorkload:
                                             max_range_tokens=int(lens.max()) if range_hints else 0,
                                             waves_hint=waves_hint, chunks_hint=chunks_hint,
                                             total_range_tokens=int(lens.sum()) if range_hints else 0,
-                                            seq_order=self._orders[-1], plan_hint=plan_hint))
+                                            seq_order=self._orders[-1], plan_hint=plan_hint,
+                                            nonempty_ranges=int(np.count_nonzero(lens)) if range_hints else 0))
         # The fused call sees each sequence's ranges as one concatenated range.
         lens_all = (w.kv_end.astype(np.int64) - w.kv_begin).sum(axis=0)
         self._orders.append(order(lens_all))
@@ -70,7 +71,8 @@ class DeviceWorkload:
                                          max_range_tokens=int(lens_all.max()) if range_hints else 0,
                                          waves_hint=waves_hint, chunks_hint=chunks_hint,
                                          total_range_tokens=int(lens_all.sum()) if range_hints else 0,
-                                         seq_order=self._orders[-1], plan_hint=plan_hint)
+                                         seq_order=self._orders[-1], plan_hint=plan_hint,
+                                         nonempty_ranges=int(np.count_nonzero(lens_all)) if range_hints else 0)
         self.fused_out = torch.empty((B, Hq, bana.HEAD_DIM), dtype=torch.float32, device=self.device)
         self.fused_lse = torch.empty((B, Hq), dtype=torch.float32, device=self.device)
         ws = max(bana.bana_decode_attn_workspace_bytes(d) for d in self.dims + [self.fused_dims]) if use_workspace else 0
@@ -103,7 +105,7 @@ class DeviceWorkload:
                 vp(self.seq_lens), vp(self.kv_begin[p]), vp(self.kv_end[p]), vp(self.out_partials[p]),
                 vp(self.lses[p]), ws_ptr, ws_bytes])
         B, Hq = self.w.batch, self.w.num_q_heads
-        self._merge_dims = bana.bana_dims(B, Hq, 1, bana.HEAD_DIM, bana.BLOCK_SIZE, 1, 1, 0, 0, 0, 0, 0, None)
+        self._merge_dims = bana.bana_dims(B, Hq, 1, bana.HEAD_DIM, bana.BLOCK_SIZE, 1, 1, 0, 0, 0, 0, 0, None, 0)
         self._merge_args = [ctypes.byref(self._merge_dims), vp(self.out_partials), vp(self.lses), self.w.n_parts,
                             vp(self.out), vp(self.lse_out)]
         self._fused_args = [ctypes.byref(self.fused_dims), vp(self.q), vp(self.k_cache), vp(self.v_cache),

@@ -404,9 +404,8 @@ def test_migration_bit_exact_and_attention_unchanged(name, part):
     B, Hq = w.batch, w.num_q_heads
     o1 = torch.empty((B, Hq, 128), dtype=torch.float32, device="cuda")
     l1 = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
-    d2 = bana.make_dims(B, Hq, w.num_kv_heads, w.max_blocks_per_seq, m.num_blocks,
-                        max_range_tokens=dw.dims[part].max_range_tokens,
-                        total_range_tokens=dw.dims[part].total_range_tokens)
+    d2 = bana.bana_dims.from_buffer_copy(dw.dims[part])  # the same plan, over the destination pool
+    d2.num_blocks = m.num_blocks
     bana.bana_decode_attn_partial(dw.q, dk, dv, dt, dw.seq_lens, dw.kv_begin[part], dw.kv_end[part], o1, l1,
                                   workspace=dw.workspace, dims=d2)
     op, lp, _, _ = dw.results()
@@ -552,8 +551,8 @@ def test_pool_beyond_4gib_uses_64bit_offsets():
     for p in range(w.n_parts):
         o = torch.empty((B, Hq, 128), dtype=torch.float32, device="cuda")
         l = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
-        d = bana.make_dims(B, Hq, 8, w.max_blocks_per_seq, big_nb, max_range_tokens=small.dims[p].max_range_tokens,
-                           total_range_tokens=small.dims[p].total_range_tokens)
+        d = bana.bana_dims.from_buffer_copy(small.dims[p])  # the same plan, over the big pools
+        d.num_blocks = big_nb
         bana.bana_decode_attn_partial(small.q, big_k, big_v, table, small.seq_lens, small.kv_begin[p],
                                       small.kv_end[p], o, l, workspace=small.workspace, dims=d)
         assert np.array_equal(o.cpu().numpy(), ref[0][p]) and np.array_equal(l.cpu().numpy(), ref[1][p])
@@ -887,3 +886,50 @@ def test_random_launch_hints_and_head_ranges(case):
         assert np.all(o[:, hs][~fin] == 0.0)
         _check_lse(l[:, hs], rl[0][:, hs], "head range lse")
         assert np.all(np.isnan(o[:, :g0 * G])) and np.all(np.isnan(o[:, g1 * G:]))
+
+
+def test_forced_balanced_launch_on_mixed():
+    """The balanced launch over all 256 sequences of the mixed workload (the schedule's prefix sums
+    span four 64-lane strides), per partition and fused, against the oracle."""
+    _full_parity(_workload("mixed"), plan_hint=2)
+
+
+@pytest.mark.parametrize("case", range(8))
+def test_random_shapes_many_sequences(case):
+    """Seeded random workloads of 65-300 sequences with uneven, empty and ragged ranges through the
+    automatic, chunked and balanced plans (the balanced schedule beyond one 64-lane stride)."""
+    rng = np.random.default_rng(90000 + case)
+    B = int(rng.integers(65, 301))
+    Hkv = int(rng.choice([1, 2, 4]))
+    Hq = Hkv * int(rng.choice([1, 4, 8]))
+    n_parts = int(rng.integers(1, 4))
+    lens = [int(x) for x in np.clip(np.rint(np.exp(rng.normal(np.log(300.0), 1.0, size=B))), 1, 4000)]
+    ranges = [[] for _ in range(n_parts)]
+    for L in lens:
+        cuts = np.sort(rng.integers(0, L + 1, size=n_parts - 1)).tolist()
+        edges = [0] + cuts + [L]
+        for p in range(n_parts):
+            ranges[p].append((edges[p], edges[p + 1]))
+    w = W.make_custom(91000 + case, B, Hq, Hkv, lens, ranges, q_scale=1 / math.sqrt(128))
+    _log(f"[many {case}] B={B} Hq={Hq} Hkv={Hkv} parts={n_parts}")
+    for plan in (0, 1, 2):
+        _full_parity(w, plan_hint=plan)
+
+
+@pytest.mark.parametrize("B", [2048, 2049])
+def test_balanced_launch_at_its_batch_limit(B):
+    """2048 sequences (the balanced schedule's limit: four per thread of the LDS scan) run the
+    balanced launch; 2049 fall back to the chunked launch.  Both against the oracle."""
+    rng = np.random.default_rng(B)
+    lens = [int(x) for x in rng.integers(1, 97, size=B)]
+    lens[5] = 3000
+    cuts = [int(rng.integers(0, L + 1)) if b % 7 else L for b, L in enumerate(lens)]  # every 7th: 2nd part empty
+    ranges = [[(0, c) for c in cuts], [(c, L) for c, L in zip(cuts, lens)]]
+    w = W.make_custom(B, B, 4, 1, lens, ranges, q_scale=1 / math.sqrt(128))
+    dw = _full_parity(w, plan_hint=2)
+    # The balanced plan has a workspace layout of its own: the forced-balanced dims size differently
+    # from the forced-chunked ones exactly when the balanced launch runs.
+    chunked = bana.bana_dims.from_buffer_copy(dw.dims[0])
+    chunked.plan_hint = 1
+    balanced_ran = bana.bana_decode_attn_workspace_bytes(dw.dims[0]) != bana.bana_decode_attn_workspace_bytes(chunked)
+    assert balanced_ran == (B <= 2048)

@@ -234,7 +234,7 @@ def test_sizes_beyond_32_bit_indices_are_unsupported(lib):
 
 
 def _balanced_bytes(B, Hq, Hkv):
-    K = max(1, 4096 // (8 * Hkv)) * 8
+    K = max(1, 2048 // (8 * Hkv)) * 8  # 2048 wavefronts over the kv heads, 8 per workgroup
     pieces = (K + B) * Hq
     lse = (pieces * 128 * 4 + 255) // 256 * 256
     prefix = (lse + pieces * 4 + 255) // 256 * 256
@@ -242,24 +242,33 @@ def _balanced_bytes(B, Hq, Hkv):
 
 
 def test_plan_choice_between_chunked_and_balanced(lib):
-    """The balanced launch is chosen for a very uneven spread over few (sequence, kv head) pairs, and
-    only there; its workspace holds K + B piece rows per query head and the prefix sums."""
+    """The balanced launch is chosen for an uneven spread over few active (sequence, kv head) pairs,
+    and only there; its workspace holds K + B piece rows per query head and the prefix sums."""
     def ws(B, Hq, Hkv, max_tok, total_tok, **kw):
         d = bana.make_dims(B, Hq, Hkv, 8192, 100000, max_range_tokens=max_tok, total_range_tokens=total_tok, **kw)
         return lib.bana_decode_attn_workspace_bytes(ctypes.byref(d))
 
     # 8 sequences, longest 3 x the mean (a long-context partition): balanced
     assert ws(8, 32, 8, 77000, 8 * 25000) == _balanced_bytes(8, 32, 8)
-    # the same with a 1.3 x spread: chunked (chunk partials [nc][B][Hq])
-    w = ws(8, 32, 8, 100000, 8 * 77000)
+    # a 1.3 x spread (long's fused call): balanced
+    assert ws(8, 32, 8, 100000, 8 * 77000) == _balanced_bytes(8, 32, 8)
+    # a 1.2 x spread: chunked (chunk partials [nc][B][Hq])
+    w = ws(8, 32, 8, 92000, 8 * 77000)
     rows = 8 * 32
     assert w != _balanced_bytes(8, 32, 8)
     assert any(w == (nc * rows * 129 * 4 + 255) // 256 * 256 for nc in range(2, 257))
     # many pairs (256 sequences x 8 kv heads), heavy tail: chunked, never balanced
     assert ws(256, 32, 8, 7568, 256 * 1400) != _balanced_bytes(256, 32, 8)
-    # batch above 64: the balanced hint falls back to the chunked plan
-    assert ws(100, 8, 2, 5000, 100 * 300, plan_hint=2) != _balanced_bytes(100, 8, 2)
-    # plan_hint 2 forces it (batch <= 64), plan_hint 1 forbids it
+    # 256 sequences x 4 kv heads (a head half of the same): 1024 pairs, balanced
+    assert ws(256, 16, 4, 7568, 256 * 1400) == _balanced_bytes(256, 16, 4)
+    # 256 sequences of which 61 have a range (a migrated partition): the active pairs decide
+    assert ws(256, 32, 8, 14000, 61 * 1400, nonempty_ranges=61) == _balanced_bytes(256, 32, 8)
+    assert ws(256, 32, 8, 14000, 61 * 1400) != _balanced_bytes(256, 32, 8)
+    # batch up to 2048 takes the balanced hint; above, it falls back to the chunked plan
+    assert ws(100, 8, 2, 5000, 100 * 300, plan_hint=2) == _balanced_bytes(100, 8, 2)
+    assert ws(2048, 8, 2, 300, 2048 * 100, plan_hint=2) == _balanced_bytes(2048, 8, 2)
+    assert ws(2049, 8, 2, 300, 2049 * 100, plan_hint=2) != _balanced_bytes(2049, 8, 2)
+    # plan_hint 2 forces it, plan_hint 1 forbids it
     assert ws(4, 8, 2, 1000, 4 * 900, plan_hint=2) == _balanced_bytes(4, 8, 2)
     assert ws(8, 32, 8, 77000, 8 * 25000, plan_hint=1) != _balanced_bytes(8, 32, 8)
     # too few blocks for one round of wavefronts: no balanced launch without the hint
