@@ -13,8 +13,8 @@ block 16, seq_len 4096, last 30 % of each sequence's blocks migrated ->
 Prints ONE JSON line.  ``value`` is the KV-read bandwidth of the whole step
 (K+V bytes of all covered tokens / step time); ``tokens_per_s`` is decode
 tokens (sequences) per second for the layer.  Every time is the median of K
-repetitions, each timed alone by HIP events on its stream with a 512 MiB cache
-scrub written before it (``timing`` gives p10 / p90); ``warm_back_to_back``
+repetitions, each timed alone by HIP events on its stream after a cache scrub
+(512 MiB written, then read back; ``timing`` gives p10 / p90); ``warm_back_to_back``
 is the same step run K times back to back with warm caches, by the host
 clock.  ``gather_read_ceiling`` reads the same
 tiles with no arithmetic (the access pattern's practical ceiling);
@@ -216,10 +216,18 @@ def main():
     from paper_2510_13223_amd import bana
 
     # Every timed figure below is taken the same way: HIP events recorded on the stream the work
-    # runs on, around each repetition alone, with a 512 MiB scrub write between repetitions
-    # (outside the events) so neither L2 nor the 256 MB last-level cache holds K/V from the
-    # previous one; the figure is the median over the K repetitions, with p10 / p90 beside it.
+    # runs on, around each repetition alone, with a cache scrub between repetitions (outside the
+    # events); the figure is the median over the K repetitions, with p10 / p90 beside it.  The
+    # scrub writes a 512 MiB buffer, so neither L2 nor the 256 MB last-level cache holds K/V from
+    # the previous repetition, then reads it back, so no dirty scrub line is left to be written
+    # back inside the timed region (measured on MI355X: a write alone adds up to 60 us of
+    # write-back to the fine workload's step).
     scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    scrub_sink = torch.empty(2048, dtype=torch.int32, device=dev)
+
+    def scrub_caches(k):
+        scrub.fill_(k & 0xFF)
+        bana.bana_debug_stream_read(scrub, scrub_sink, stream=stream)
 
     def timed_cold(fn, inner=None):
         """Event-timed repetitions of fn with a scrub before each; returns us per repetition
@@ -229,7 +237,7 @@ def main():
         torch.cuda.synchronize()
         with torch.cuda.stream(stream):
             for k in range(args.steps):
-                scrub.fill_(k & 0xFF)
+                scrub_caches(k)
                 ev[k][0].record(stream)
                 fn()
                 ev[k][1].record(stream)
@@ -295,14 +303,14 @@ def main():
     torch.cuda.synchronize()
     with torch.cuda.stream(stream):
         for k in range(args.steps):
-            scrub.fill_(k & 0xFF)
+            scrub_caches(k)
             ev_all[k][0].record(stream)
             for p in range(P):
                 dw.partial(p, h)
             ev_all[k][1].record(stream)
             dw.merge(h)
         for k in range(args.steps):
-            scrub.fill_(k & 0xFF)
+            scrub_caches(k)
             for p in range(P):
                 ev[k][p][0].record(stream)
                 dw.partial(p, h)
@@ -398,8 +406,8 @@ def main():
         "data": "synthetic",
         "config": _workload_desc(w),
         "timing": {
-            "method": "HIP events around each step alone on its stream, 512 MiB scrub write between steps "
-                      "(outside the events); value and ms_per_step from the median",
+            "method": "HIP events around each step alone on its stream; between steps (outside the events) "
+                      "a 512 MiB scrub written then read back; value and ms_per_step from the median",
             **stats(step_us),
         },
         "frac_of_hbm_peak": round(kv_bytes / t_step / 1e9 / HBM_PEAK_GBS, 4),

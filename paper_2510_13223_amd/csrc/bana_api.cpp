@@ -65,6 +65,7 @@ struct Plan {
   bool balanced;  // equal block intervals per wavefront across sequences
   int K;          // balanced: wavefronts per kv head
   int kp;         // balanced: thread groups per row of the piece merge
+  bool ordered;   // follow the caller's dispatch order (uneven ranges only)
 };
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
@@ -114,6 +115,10 @@ Plan make_plan(const bana_dims* d) {
   const bool uneven = hinted && 4 * bound > 5 * mean_blocks;
   Plan p;
   p.balanced = false;
+  // The dispatch order pays off only when ranges are uneven (long ones first, short ones
+  // filling the end of the launch); with even or unknown lengths its lookup would add one
+  // dependent load to every wavefront's start, so it is skipped.
+  p.ordered = uneven;
   p.K = std::max(1, kBalancedTargetWaves / (bana::kBalancedWaves * d->num_kv_heads)) * bana::kBalancedWaves;
   p.kp = 1;
   // The balanced schedule counts the blocks of all ranges of all sequences in 32 bits.
@@ -272,7 +277,7 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
   a.begin = kv_range_begin;
   a.end = kv_range_end;
   a.n_parts = n_parts;
-  a.seq_order = d->seq_order;
+  a.seq_order = plan.ordered ? d->seq_order : nullptr;
   a.B = d->batch;
   a.Hq = d->num_q_heads;
   a.Hkv = d->num_kv_heads;

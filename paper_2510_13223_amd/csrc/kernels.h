@@ -60,7 +60,10 @@ hipError_t launch_merge(const float* outs, const float* lses, int n_parts, Merge
                         hipStream_t stream);
 
 // Copy of the K/V tiles (all kv heads) of logical blocks [blk_begin[b], blk_end[b]) from the
-// src pool (src_table) to the dst pool (dst_table); grid covers max_migrated_blocks per sequence.
+// src pool (src_table) to the dst pool (dst_table); max_migrated_blocks bounds blk_end - blk_begin.
+// Up to kMaxFlatMigrateBatch sequences: one flat list of tiles over a round of resident
+// workgroups; more: a grid row per sequence.
+constexpr int kMaxFlatMigrateBatch = 4096;
 hipError_t launch_migrate(const void* src_k, const void* src_v, const int32_t* src_table, void* dst_k, void* dst_v,
                           const int32_t* dst_table, const int32_t* blk_begin, const int32_t* blk_end, int B,
                           int max_blocks, int max_migrated_blocks, int Hkv, hipStream_t stream);

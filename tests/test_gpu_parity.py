@@ -933,3 +933,45 @@ def test_balanced_launch_at_its_batch_limit(B):
     chunked.plan_hint = 1
     balanced_ran = bana.bana_decode_attn_workspace_bytes(dw.dims[0]) != bana.bana_decode_attn_workspace_bytes(chunked)
     assert balanced_ran == (B <= 2048)
+
+
+def _migrate_and_check(w, part, seed, hint=True):
+    m = W.make_migration(w, part, seed=seed)
+    dk = torch.from_numpy(m.dst_k.view(np.int16)).view(torch.bfloat16).cuda()
+    dv = torch.from_numpy(m.dst_v.view(np.int16)).view(torch.bfloat16).cuda()
+    i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    hint_tokens = int(np.max(m.blk_end - m.blk_begin)) * 16 if hint else 0
+    bana.bana_migrate_kv_blocks(bf(w.k_cache), bf(w.v_cache), i32(w.block_table), dk, dv, i32(m.dst_table),
+                                i32(m.blk_begin), i32(m.blk_end), max_range_tokens=hint_tokens)
+    ek, ev = oracle.migrate(w.k_cache, w.v_cache, w.block_table, m.dst_k, m.dst_v, m.dst_table, m.blk_begin,
+                            m.blk_end)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(dk.cpu().view(torch.int16).numpy().view(np.uint16), ek)
+    np.testing.assert_array_equal(dv.cpu().view(torch.int16).numpy().view(np.uint16), ev)
+
+
+@pytest.mark.parametrize("case", range(10))
+def test_migration_random_batches_bit_exact(case):
+    """The flat migration (blocks of all sequences in one list, split evenly over the workgroups)
+    on seeded random batches of 1-300 sequences, 1-8 kv heads, many empty ranges, against the
+    oracle's copy bit for bit (every destination block outside the list keeps its sentinel)."""
+    rng = np.random.default_rng(120000 + case)
+    B = int(rng.integers(1, 301))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    lens = [int(x) for x in rng.integers(1, 700, size=B)]
+    cuts = [int(rng.integers(0, L + 1)) if rng.random() < 0.6 else L for L in lens]
+    ranges = [[(0, c) for c in cuts], [(c, L) for c, L in zip(cuts, lens)]]
+    w = W.make_custom(121000 + case, B, Hkv, Hkv, lens, ranges)
+    _log(f"[migrate random {case}] B={B} Hkv={Hkv}")
+    _migrate_and_check(w, 1, seed=case, hint=bool(case % 2))
+
+
+def test_migration_beyond_the_flat_batch_limit():
+    """5000 sequences (above the flat list's 4096): the per-sequence grid, bit for bit."""
+    B = 5000
+    rng = np.random.default_rng(5000)
+    lens = [int(x) for x in rng.integers(1, 80, size=B)]
+    cuts = [int(rng.integers(0, L + 1)) for L in lens]
+    w = W.make_custom(5000, B, 2, 2, lens, [[(0, c) for c in cuts], [(c, L) for c, L in zip(cuts, lens)]])
+    _migrate_and_check(w, 1, seed=1)
