@@ -16,7 +16,8 @@ from typing import Optional
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libbana.so")
+LIB_PATH = os.environ.get("BANA_LIBRARY") or os.path.join(_PKG, "libbana.so")
+RACECHECK_LIB_PATH = os.path.join(_PKG, "libbana_racecheck.so")
 
 HEAD_DIM = 128
 BLOCK_SIZE = 16
@@ -61,11 +62,17 @@ _lib = None
 def lib() -> ctypes.CDLL:
     """The loaded libbana.so (raises if it has not been built)."""
     global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(LIB_PATH):
-        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2510_13223_amd.build`")
-    L = ctypes.CDLL(LIB_PATH)
+    if _lib is None:
+        _lib = load(LIB_PATH)
+    return _lib
+
+
+def load(path: str) -> ctypes.CDLL:
+    """A build of the library at ``path`` with the C ABI's argument types set (raises if missing).
+    Loaded with local symbol scope, so a second build (the LDS race-check one) keeps its own code."""
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2510_13223_amd.build`")
+    L = ctypes.CDLL(path, mode=os.RTLD_LOCAL | os.RTLD_NOW)
     P = ctypes.c_void_p
     D = ctypes.POINTER(bana_dims)
     L.bana_decode_attn_partial.argtypes = [D, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
@@ -97,7 +104,6 @@ def lib() -> ctypes.CDLL:
     L.bana_debug_gather_read.restype = ctypes.c_int
     L.bana_debug_stream_read.argtypes = [P, ctypes.c_size_t, ctypes.c_int32, P, P]
     L.bana_debug_stream_read.restype = ctypes.c_int
-    _lib = L
     return L
 
 

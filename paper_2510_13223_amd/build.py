@@ -45,9 +45,12 @@ def _compile(src: str, verbose: bool, build_dir: str, defines) -> str:
     return obj
 
 
+RACECHECK_LIB = os.path.join(PKG, "libbana_racecheck.so")
+
+
 def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
-    """Compile and link; ``out`` / ``defines`` allow side builds with tuning macros."""
-    build_dir = BUILD if out == LIB else out + ".objs"
+    """Compile and link; ``out`` / ``defines`` allow side builds with other macros."""
+    build_dir = BUILD if out == LIB else os.path.join(BUILD, os.path.basename(out) + ".objs")
     os.makedirs(build_dir, exist_ok=True)
     with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose, build_dir, defines), SOURCES))
@@ -62,5 +65,12 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
     return out
 
 
+def build_racecheck(verbose: bool = False) -> str:
+    """The LDS race-check build (BANA_LDS_RACE_CHECK): delayed LDS writers and an extra barrier
+    before every LDS read-back; a GPU test requires its results to equal the product build's."""
+    return build(verbose, out=RACECHECK_LIB, defines=("BANA_LDS_RACE_CHECK",))
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
+    print(build_racecheck(verbose="-v" in sys.argv))

@@ -368,6 +368,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   float* sm_m = smem;               // [W][16]
   float* sm_l = smem + 16 * W;      // [W][16]
   float* sm_acc = smem + 32 * W;    // [W][G][kRowPad]
+  race_check_delay(wave);
   if (quad == 0) {
     sm_m[wave * 16 + col] = st.m;   // -inf for a wave that saw no block
     sm_l[wave * 16 + col] = lsum;
@@ -378,6 +379,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
       *reinterpret_cast<f32x4*>(sm_acc + (wave * G + col) * kRowPad + 16 * dt + 4 * quad) = st.acc[dt];
   }
   __syncthreads();
+  race_check_barrier();
   for (int idx = threadIdx.x; idx < G * (kHeadDim / 4); idx += 64 * W) {
     const int h = idx >> 5;
     const int d4 = idx & 31;
@@ -448,10 +450,13 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     const int y = __shfl_up(incl, off);
     if (lane >= off) incl += y;
   }
+  race_check_delay(wave);
   if (lane == 63) sm_wave_sum[wave] = incl;
   __syncthreads();
+  race_check_barrier();
   int before = incl - local;
   for (int w = 0; w < wave; ++w) before += sm_wave_sum[w];
+  race_check_delay(wave);
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i) {
     const int b = s0 + i;
@@ -459,6 +464,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     if (i < per && b < B) sm_incl[b] = before;
   }
   __syncthreads();
+  race_check_barrier();
 
   if (blockIdx.x == 0) {
     for (int i = threadIdx.x; i <= B; i += kThreads) prefix[i] = i == 0 ? 0 : sm_incl[i - 1];

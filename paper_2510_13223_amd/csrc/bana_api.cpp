@@ -105,13 +105,17 @@ Plan make_plan(const bana_dims* d) {
   const int64_t active = d->nonempty_ranges > 0 ? std::min<int64_t>(d->nonempty_ranges, d->batch) : d->batch;
   const int64_t active_pairs = active * d->num_kv_heads;
   int64_t bound = d->max_blocks_per_seq;  // blocks of the longest range
-  if (d->max_range_tokens > 0) bound = std::min<int64_t>(bound, (d->max_range_tokens + kBlockSize - 1) / kBlockSize);
+  if (d->max_range_tokens > 0)
+    bound = std::min<int64_t>(bound, ((int64_t)d->max_range_tokens + kBlockSize - 1) / kBlockSize);
   bound = std::max<int64_t>(bound, 1);
   int64_t wpp = (kTargetWaves + active_pairs - 1) / active_pairs;
   wpp = std::max<int64_t>(1, std::min<int64_t>(wpp, std::max<int64_t>(1, bound / kMinBlocksPerWave)));
   const bool hinted = d->total_range_tokens > 0;
+  // The mean range cannot exceed the longest one; hints that say otherwise are clamped (this
+  // also keeps mean_blocks x pairs inside 64 bits).
   const int64_t mean_blocks =
-      hinted ? std::max<int64_t>(1, d->total_range_tokens / (kBlockSize * active) + 1) : bound;
+      hinted ? std::max<int64_t>(1, std::min<int64_t>(bound + 1, d->total_range_tokens / (kBlockSize * active) + 1))
+             : bound;
   const bool uneven = hinted && 4 * bound > 5 * mean_blocks;
   Plan p;
   p.balanced = false;
@@ -453,7 +457,8 @@ bana_status bana_migrate_kv_blocks(const bana_dims* d, const void* src_k_cache, 
   if (d->batch > 65535) return BANA_ERR_UNSUPPORTED;  // one grid row per sequence
   // Blocks per sequence the grid must cover: the hint (in tokens) when given, else the table width.
   int64_t maxb = d->max_blocks_per_seq;
-  if (d->max_range_tokens > 0) maxb = std::min<int64_t>(maxb, (d->max_range_tokens + kBlockSize - 1) / kBlockSize);
+  if (d->max_range_tokens > 0)
+    maxb = std::min<int64_t>(maxb, ((int64_t)d->max_range_tokens + kBlockSize - 1) / kBlockSize);
   return device_status(bana::launch_migrate(src_k_cache, src_v_cache, src_block_table, dst_k_cache, dst_v_cache,
                                             dst_block_table, blk_begin, blk_end, d->batch, d->max_blocks_per_seq,
                                             (int)maxb, d->num_kv_heads, static_cast<hipStream_t>(stream)));

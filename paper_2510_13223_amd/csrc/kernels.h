@@ -9,6 +9,20 @@
 
 namespace bana {
 
+// LDS race check (a build option for a test build only): before writing what other wavefronts of
+// the workgroup read back through LDS, odd wavefronts sleep a few microseconds, and every
+// read-back is preceded by one more barrier.  With the barriers the kernels already have, results
+// must not change bit for bit; a read that raced a write would change them.
+#ifdef BANA_LDS_RACE_CHECK
+__device__ __forceinline__ void race_check_delay(int wave) {
+  if (wave & 1) __builtin_amdgcn_s_sleep(127);
+}
+__device__ __forceinline__ void race_check_barrier() { __syncthreads(); }
+#else
+__device__ __forceinline__ void race_check_delay(int) {}
+__device__ __forceinline__ void race_check_barrier() {}
+#endif
+
 struct PartialArgs {
   const uint16_t* q;        // bf16 [B][Hq][128]
   const uint16_t* k;        // bf16 [num_blocks][Hkv][128/8][16][8]

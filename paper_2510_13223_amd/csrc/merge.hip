@@ -179,12 +179,14 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
   }
   float M = m;
   if (KP > 1) {
+    race_check_delay(t >> 6);
     sm_acc[(rl * KP + k) * 32 + d4] = acc;
     if (d4 == 0) {
       sm_m[rl * KP + k] = m;
       sm_w[rl * KP + k] = wsum;
     }
     __syncthreads();
+    race_check_barrier();
     if (k != 0) return;
     M = -INFINITY;
 #pragma unroll

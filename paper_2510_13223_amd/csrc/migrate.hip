@@ -113,10 +113,13 @@ __global__ __launch_bounds__(kThreads) void migrate_flat_kernel(const u32x4* __r
     const int y = __shfl_up(incl, off);
     if (lane >= off) incl += y;
   }
+  race_check_delay(wave);
   if (lane == 63) sm_wave_sum[wave] = incl;
   __syncthreads();
+  race_check_barrier();
   int before = incl - local;
   for (int w = 0; w < wave; ++w) before += sm_wave_sum[w];
+  race_check_delay(wave);
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i) {
     const int b = s0 + i;
@@ -124,6 +127,7 @@ __global__ __launch_bounds__(kThreads) void migrate_flat_kernel(const u32x4* __r
     if (i < per && b < B) sm_incl[b] = before;
   }
   __syncthreads();
+  race_check_barrier();
 
   const int tpb = 2 * Hkv;                                   // tiles per block
   const int64_t n_tiles = (int64_t)sm_incl[B - 1] * tpb;

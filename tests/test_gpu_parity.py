@@ -9,6 +9,7 @@ oracle's, zero keys give round(exp(lse)) == range length, and a dominant key
 returns its value row exactly.
 """
 
+import ctypes
 import dataclasses
 import math
 import sys
@@ -975,3 +976,52 @@ def test_migration_beyond_the_flat_batch_limit():
     cuts = [int(rng.integers(0, L + 1)) for L in lens]
     w = W.make_custom(5000, B, 2, 2, lens, [[(0, c) for c in cuts], [(c, L) for c, L in zip(cuts, lens)]])
     _migrate_and_check(w, 1, seed=1)
+
+
+def _raw_step(L, dw, h):
+    """Every partition, the merge and the fused call of a prepared workload through library L."""
+    for p in range(dw.w.n_parts):
+        assert L.bana_decode_attn_partial(*dw._partial_args[p], h) == bana.BANA_OK
+    assert L.bana_merge_partials(*dw._merge_args, h) == bana.BANA_OK
+    assert L.bana_decode_attn_fused(*dw._fused_args, h) == bana.BANA_OK
+
+
+@pytest.mark.parametrize("name,plan", [("tiny", 0), ("tiny", 2), ("fine", 0), ("llama3_8b", 0), ("mixed", 0)])
+def test_lds_race_check_build_bit_identical(name, plan):
+    """The LDS race-check build (odd wavefronts sleep before every LDS write that other wavefronts
+    read back, and one more barrier precedes every read-back) gives the product build's results bit
+    for bit: the cross-wave combine of the chunked launch (llama3_8b, mixed), the balanced launch's
+    prefix scan and the piece merge's thread-group combine (tiny forced balanced, mixed's migrated
+    partition), and the flat migration's scan."""
+    side = bana.load(bana.RACECHECK_LIB_PATH)
+    with open(bana.RACECHECK_LIB_PATH, "rb") as f1, open(bana.LIB_PATH, "rb") as f2:
+        assert f1.read() != f2.read(), "the race-check build must differ from the product build"
+    w = _workload(name)
+    dw = DeviceWorkload(w, plan_hint=plan)
+    h = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    outs = (dw.out_partials, dw.lses, dw.out, dw.lse_out, dw.fused_out, dw.fused_lse)
+    _raw_step(bana.lib(), dw, h)
+    ref = [t.clone() for t in outs]
+    for t in outs:
+        t.fill_(float("nan"))
+    _raw_step(side, dw, h)
+    torch.cuda.synchronize()
+    for a, b in zip(outs, ref):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    # the flat migration of the last partition
+    m = W.make_migration(w, w.n_parts - 1, seed=3)
+    i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+    dst = []
+    for L in (bana.lib(), side):
+        dk = torch.from_numpy(m.dst_k.view(np.int16)).view(torch.bfloat16).cuda()
+        dv = torch.from_numpy(m.dst_v.view(np.int16)).view(torch.bfloat16).cuda()
+        dt, mb, me = i32(m.dst_table), i32(m.blk_begin), i32(m.blk_end)
+        d = bana.bana_dims(w.batch, w.num_kv_heads, w.num_kv_heads, 128, 16, w.max_blocks_per_seq, w.num_blocks,
+                           0, 0, 0, 0, 0, None, 0)
+        vp = lambda t: ctypes.c_void_p(t.data_ptr())
+        assert L.bana_migrate_kv_blocks(ctypes.byref(d), vp(dw.k_cache), vp(dw.v_cache), vp(dw.block_table), vp(dk),
+                                        vp(dv), vp(dt), m.num_blocks, vp(mb), vp(me), h) == bana.BANA_OK
+        torch.cuda.synchronize()
+        dst.append((dk, dv))
+    assert torch.equal(dst[0][0].view(torch.int16), dst[1][0].view(torch.int16))
+    assert torch.equal(dst[0][1].view(torch.int16), dst[1][1].view(torch.int16))
