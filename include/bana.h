@@ -233,6 +233,40 @@ bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void
                                    float* out, float* lse_out, void* workspace, size_t workspace_bytes,
                                    void* stream);
 
+/* One host <-> device copy (see bana_decode_attn_fused_copies). */
+typedef struct {
+  void* dst;       /* device or pinned host memory, 16-byte aligned */
+  const void* src; /* device or pinned host memory, 16-byte aligned */
+  size_t bytes;    /* a multiple of 16 */
+} bana_copy;
+
+/*
+ * bana_decode_attn_fused with up to 8 copies carried by the same launch: the
+ * layer-wise pipeline of Sec. 4.2, where the fetch of layer i+1's KV from
+ * the host store and the store of layer i-1's KV back to it overlap the
+ * attention of layer i.  The copies (each like bana_copy_async) run in the
+ * launch's first workgroups, dispatched ahead of the attention's, so one
+ * launch per layer on one stream overlaps all three stages and orders them
+ * against the neighbouring layers' launches by the stream alone.  The
+ * attention runs the chunked launch (as with plan_hint 1) and its results
+ * equal bana_decode_attn_fused with plan_hint 1 bit for bit.  The copies must
+ * not overlap one another or any buffer the attention reads or writes.  The
+ * copy workgroups take CU slots first: a plan that fills a whole dispatch round
+ * by itself then runs some attention workgroups in a second round, so such
+ * callers pass waves_hint 4 (or fewer) to leave room.  workspace: as for the
+ * fused call, sized by bana_decode_attn_workspace_bytes of d with plan_hint 1.
+ * A zero-byte copy is skipped (its pointers are not looked at).  Errors as for
+ * the fused call; more than 8 copies gives BANA_ERR_UNSUPPORTED, a copy of a
+ * non-zero size with a NULL or misaligned pointer or a size that is not a
+ * multiple of 16 BANA_ERR_INVALID.
+ */
+bana_status bana_decode_attn_fused_copies(const bana_dims* d, const void* q, const void* k_cache,
+                                          const void* v_cache, const int32_t* block_table, const int32_t* seq_lens,
+                                          const int32_t* kv_range_begin, const int32_t* kv_range_end,
+                                          int32_t n_parts, float* out, float* lse_out, void* workspace,
+                                          size_t workspace_bytes, const bana_copy* copies, int32_t n_copies,
+                                          void* stream);
+
 /*
  * Merge of n_parts partials (Sec. 4.1(2), final O = O^(1) + O^(2) with the
  * exchange of the partial denominators l^(j) = exp(lse_j)).  Per row

@@ -47,6 +47,10 @@ class bana_dims(ctypes.Structure):
     ]
 
 
+class bana_copy(ctypes.Structure):
+    _fields_ = [("dst", ctypes.c_void_p), ("src", ctypes.c_void_p), ("bytes", ctypes.c_size_t)]
+
+
 class BanaError(RuntimeError):
     def __init__(self, status: int, what: str, detail: str = ""):
         self.status = status
@@ -83,6 +87,9 @@ def load(path: str) -> ctypes.CDLL:
     L.bana_decode_attn_workspace_bytes.restype = ctypes.c_size_t
     L.bana_decode_attn_fused.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_int32, P, P, P, ctypes.c_size_t, P]
     L.bana_decode_attn_fused.restype = ctypes.c_int
+    L.bana_decode_attn_fused_copies.argtypes = [D, P, P, P, P, P, P, P, ctypes.c_int32, P, P, P, ctypes.c_size_t,
+                                                ctypes.POINTER(bana_copy), ctypes.c_int32, P]
+    L.bana_decode_attn_fused_copies.restype = ctypes.c_int
     L.bana_merge_partials.argtypes = [D, P, P, ctypes.c_int32, P, P, P]
     L.bana_merge_partials.restype = ctypes.c_int
     L.bana_status_string.argtypes = [ctypes.c_int]
@@ -283,6 +290,52 @@ def bana_decode_attn_fused(q, k_cache, v_cache, block_table, seq_lens, kv_range_
         _stream(stream))
     if st != BANA_OK:
         raise BanaError(st, "bana_decode_attn_fused")
+
+
+def copy_list(copies) -> "ctypes.Array":
+    """A bana_copy array from (dst tensor, src tensor) pairs (each contiguous, device or pinned host
+    memory, the same number of bytes, a multiple of 16)."""
+    arr = (bana_copy * len(copies))()
+    for i, (dst, src) in enumerate(copies):
+        for t, name in ((dst, "dst"), (src, "src")):
+            if not isinstance(t, torch.Tensor) or not t.is_contiguous():
+                raise ValueError(f"copy {i}: {name} must be a contiguous tensor")
+            if t.device.type != "cuda" and not t.is_pinned():
+                raise ValueError(f"copy {i}: {name} must be device or pinned host memory")
+        nbytes = src.numel() * src.element_size()
+        if dst.numel() * dst.element_size() != nbytes:
+            raise ValueError(f"copy {i}: dst and src differ in size")
+        arr[i] = bana_copy(dst.data_ptr(), src.data_ptr(), nbytes)
+    return arr
+
+
+def bana_decode_attn_fused_copies(q, k_cache, v_cache, block_table, seq_lens, kv_range_begin, kv_range_end, out,
+                                  lse_out, copies=(), workspace: Optional[torch.Tensor] = None, stream=None,
+                                  dims: Optional[bana_dims] = None) -> None:
+    """The fused call with up to 8 (dst, src) copies carried by the same launch; see include/bana.h."""
+    B, Hq, D = _check_attn_inputs(q, k_cache, v_cache, block_table, seq_lens)
+    if kv_range_begin.dim() != 2 or kv_range_begin.shape[1] != B:
+        raise ValueError("kv_range_begin must be [n_parts, B]")
+    n = kv_range_begin.shape[0]
+    _need(kv_range_begin, "kv_range_begin", torch.int32, (n, B))
+    _need(kv_range_end, "kv_range_end", torch.int32, (n, B))
+    _need(out, "out", torch.float32, (B, Hq, D))
+    _need(lse_out, "lse_out", torch.float32, (B, Hq))
+    _same_device(q, kv_range_begin, kv_range_end, out, lse_out, workspace)
+    ws_bytes = 0
+    if workspace is not None:
+        _need(workspace, "workspace", workspace.dtype)
+        ws_bytes = workspace.numel() * workspace.element_size()
+    if dims is None:
+        dims = dims_for(q, k_cache, block_table)
+    _check_dims(dims, q, k_cache, block_table)
+    arr = copy_list(list(copies))
+    st = lib().bana_decode_attn_fused_copies(
+        ctypes.byref(dims), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(seq_lens),
+        _ptr(kv_range_begin), _ptr(kv_range_end), n, _ptr(out), _ptr(lse_out), _ptr(workspace), ws_bytes, arr,
+        len(arr), _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_decode_attn_fused_copies")
 
 
 def bana_decode_attn_heads(q, k_cache, v_cache, block_table, seq_lens, kv_range_begin, kv_range_end,

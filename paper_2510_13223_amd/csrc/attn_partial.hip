@@ -310,6 +310,35 @@ __device__ __forceinline__ void walk_blocks(Online& st, const bf16x8 (&qop)[4], 
   st.update(block_scores(qop, kr), vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1, quad);
 }
 
+// Side copies: copy k is moved by the copy workgroups wg with wg % n == k, so all copies (host to
+// device and device to host alike) proceed at the same time, each direction of the host link
+// busy at once.  Within copy k, workgroup j of its m workgroups moves 16-byte units
+// j * threads + tid, advancing by m * threads, kSideCopyUnroll units in flight per thread.  Either side may be
+// device memory or pinned host memory; the source is read once (non-temporal), the destination is
+// not read back by this launch (non-temporal stores).
+constexpr int kSideCopyUnroll = 1;  // 16-byte units in flight per thread of a copy workgroup
+
+__device__ __forceinline__ void side_copy(const SideCopies& c, int wg, int tid, int threads) {
+  const int k = wg % c.n;
+  const int m = (c.n_wg - k + c.n - 1) / c.n;  // workgroups of copy k
+  const int64_t stride = (int64_t)m * threads;
+  const int64_t first = (int64_t)(wg / c.n) * threads + tid;
+  {
+    const u32x4* __restrict__ src = static_cast<const u32x4*>(c.src[k]);
+    u32x4* __restrict__ dst = static_cast<u32x4*>(c.dst[k]);
+    const int64_t n = c.n16[k];
+    for (int64_t i0 = first; i0 < n; i0 += kSideCopyUnroll * stride) {
+      u32x4 x[kSideCopyUnroll];
+#pragma unroll
+      for (int u = 0; u < kSideCopyUnroll; ++u)
+        if (i0 + u * stride < n) x[u] = __builtin_nontemporal_load(src + i0 + u * stride);
+#pragma unroll
+      for (int u = 0; u < kSideCopyUnroll; ++u)
+        if (i0 + u * stride < n) __builtin_nontemporal_store(x[u], dst + i0 + u * stride);
+    }
+  }
+}
+
 // MULTI: the call passes several ranges per sequence (the fused entry point); a
 // single range (one partition) compiles the segment handling away.
 template <int W, bool MULTI>
@@ -321,7 +350,11 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   const int col = lane & 15;  // query head in group (score/output column); token row for K; dim for V
   const int quad = lane >> 4;
 
-  int wg = blockIdx.x;
+  if (blockIdx.x < (unsigned)a.copies.n_wg) {  // side-copy workgroups come first
+    side_copy(a.copies, blockIdx.x, threadIdx.x, 64 * W);
+    return;
+  }
+  int wg = blockIdx.x - a.copies.n_wg;
   const int g = a.g0 + wg % a.ng;
   wg /= a.ng;
   // The dispatch order is a hint: an entry outside [0, B) is clamped, never followed.
@@ -509,7 +542,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
 }  // namespace
 
 hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stream) {
-  const unsigned nwg = (unsigned)a.nc * (unsigned)a.B * (unsigned)a.ng;
+  const unsigned nwg = (unsigned)a.copies.n_wg + (unsigned)a.nc * (unsigned)a.B * (unsigned)a.ng;
   const size_t smem = waves > 1 ? sizeof(float) * (size_t)(32 * waves + waves * a.G * kRowPad) : 0;
   const bool multi = a.n_parts > 1;
   switch (waves) {

@@ -30,6 +30,12 @@ constexpr int kMinBlocksPerWave = 8;    // below this a wavefront spends more ti
 constexpr int kMaxBlocksPerWave = 64;   // longest run of blocks one wavefront should walk (no hints)
 constexpr int kMaxChunks = 256;
 constexpr int kMaxFusedParts = 64;  // one range per lane of the segment table
+// Workgroups of an attention launch given to its side copies.  Measured on MI355X (the llama3_8b
+// layer pipeline, 4 MiB of copies beside 1 GiB of attention reads): the copies' host-memory
+// requests slow the attention they run beside, so fewer requests in flight over the attention's
+// duration cost less: 32 workgroups with one 16-byte unit in flight per thread 0.182 ms per
+// layer, 16 or 64 of them 0.185 / 0.191 ms, four units in flight 0.188-0.243 ms.
+constexpr int kMaxSideCopyGroups = 32;
 constexpr int64_t kMaxRows = int64_t{1} << 26;  // batch x num_q_heads: 64 threads per row stay below 2^32
 constexpr int64_t kMaxLaunchItems = UINT32_MAX;  // work-items of one launch (grid x workgroup size)
 
@@ -158,7 +164,7 @@ Plan make_plan(const bana_dims* d) {
   // The cross-wave combine keeps W * G rows of 132 floats in LDS; stay within 64 KiB per workgroup.
   const int G = d->num_q_heads / d->num_kv_heads;
   while (p.waves > 1 && sizeof(float) * (size_t)(32 * p.waves + p.waves * G * (kHeadDim + 4)) > 65536) p.waves /= 2;
-  while (p.waves > 1 && pairs * 64 * p.waves > kMaxLaunchItems) p.waves /= 2;
+  while (p.waves > 1 && (pairs + kMaxSideCopyGroups) * 64 * p.waves > kMaxLaunchItems) p.waves /= 2;
   if (d->chunks_hint > 0) {
     p.nc = d->chunks_hint;
     p.cmin = 1;
@@ -186,7 +192,7 @@ Plan make_plan(const bana_dims* d) {
     p.cmin = p.waves * 16;
   }
   p.nc = std::max(1, std::min(p.nc, kMaxChunks));
-  if ((int64_t)p.nc * pairs * 64 * p.waves > kMaxLaunchItems) p.nc = 1;
+  if (((int64_t)p.nc * pairs + kMaxSideCopyGroups) * 64 * p.waves > kMaxLaunchItems) p.nc = 1;
   return p;
 }
 
@@ -258,11 +264,12 @@ namespace {
 bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,
                           const int32_t* block_table, const int32_t* kv_range_begin, const int32_t* kv_range_end,
                           int n_parts, int g0, int ng, float* out, float* lse, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+                          size_t workspace_bytes, void* stream, const bana::SideCopies* side = nullptr) {
   const int G = d->num_q_heads / d->num_kv_heads;
   bana_dims sub = *d;
   sub.num_kv_heads = ng;
   sub.num_q_heads = ng * G;
+  if (side != nullptr && side->n > 0) sub.plan_hint = 1;  // side copies ride on the chunked launch
   Plan plan = make_plan(&sub);
   const WorkspaceLayout ws = layout_for(&sub, plan);
   if (ws.total > 0 && (workspace == nullptr || workspace_bytes < ws.total)) {
@@ -294,6 +301,24 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
   // Workspace partials hold the call's heads only; merged rows go to their place in out / lse.
   a.out_hq = ng * G;
   a.out_h0 = g0 * G;
+  a.copies = bana::SideCopies{};
+  if (side != nullptr && side->n > 0) {
+    // Enough copy workgroups for the bytes (one 16-byte unit per thread per step), at most
+    // kMaxSideCopyGroups, and at least one per copy (copy k takes the workgroups wg with
+    // wg % n == k).
+    a.copies = *side;
+    int64_t units = 0;
+    for (int i = 0; i < side->n; ++i) units += side->n16[i];
+    const int64_t per_wg = (int64_t)64 * plan.waves;
+    a.copies.n_wg = (int)std::max<int64_t>(
+        side->n, std::min<int64_t>(kMaxSideCopyGroups, (units + per_wg - 1) / per_wg));
+    // The launch counts its work-items in 32 bits (only batches of nearly 2^26 (sequence, kv head)
+    // pairs come close).
+    if (((int64_t)plan.nc * d->batch * ng + a.copies.n_wg) * 64 * plan.waves > kMaxLaunchItems) {
+      g_last_error = "bana_decode_attn_fused_copies: the copy workgroups would take the launch past 2^32 work-items";
+      return BANA_ERR_UNSUPPORTED;
+    }
+  }
   bana::MergeRows m;
   m.B = d->batch;
   m.hn = ng * G;
@@ -405,6 +430,36 @@ bana_status bana_decode_attn_fused(const bana_dims* d, const void* q, const void
     return BANA_ERR_INVALID;
   return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts, 0,
                        d->num_kv_heads, out, lse_out, workspace, workspace_bytes, stream);
+}
+
+bana_status bana_decode_attn_fused_copies(const bana_dims* d, const void* q, const void* k_cache,
+                                          const void* v_cache, const int32_t* block_table, const int32_t* seq_lens,
+                                          const int32_t* kv_range_begin, const int32_t* kv_range_end,
+                                          int32_t n_parts, float* out, float* lse_out, void* workspace,
+                                          size_t workspace_bytes, const bana_copy* copies, int32_t n_copies,
+                                          void* stream) {
+  const bana_status st = check_dims(d);
+  if (st != BANA_OK) return st;
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !kv_range_begin || !kv_range_end || !out ||
+      !lse_out || n_parts < 1 || n_copies < 0 || (n_copies > 0 && copies == nullptr))
+    return BANA_ERR_INVALID;
+  if (n_parts > kMaxFusedParts || n_copies > bana::kMaxSideCopies) return BANA_ERR_UNSUPPORTED;
+  if ((int64_t)n_parts * d->max_blocks_per_seq > INT32_MAX) return BANA_ERR_UNSUPPORTED;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out) ||
+      (workspace != nullptr && !aligned16(workspace)))
+    return BANA_ERR_INVALID;
+  bana::SideCopies side{};
+  for (int i = 0; i < n_copies; ++i) {
+    const bana_copy& c = copies[i];
+    if (c.bytes == 0) continue;  // nothing to move; its pointers are not looked at
+    if (!c.dst || !c.src || c.bytes % 16 != 0 || !aligned16(c.dst) || !aligned16(c.src)) return BANA_ERR_INVALID;
+    side.src[side.n] = c.src;
+    side.dst[side.n] = c.dst;
+    side.n16[side.n] = (int64_t)(c.bytes / 16);
+    ++side.n;
+  }
+  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts, 0,
+                       d->num_kv_heads, out, lse_out, workspace, workspace_bytes, stream, &side);
 }
 
 bana_status bana_decode_attn_heads(const bana_dims* d, const void* q, const void* k_cache, const void* v_cache,

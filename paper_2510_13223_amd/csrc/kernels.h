@@ -23,6 +23,18 @@ __device__ __forceinline__ void race_check_delay(int) {}
 __device__ __forceinline__ void race_check_barrier() {}
 #endif
 
+// Host <-> device copies carried by extra workgroups of an attention launch: they take the
+// launch's first n_wg workgroups, so they are dispatched before the attention's and run beside
+// them (the layer-wise pipeline's fetch and store, inside the attention launch of a layer).
+constexpr int kMaxSideCopies = 8;
+struct SideCopies {
+  int n;     // copies (0: none)
+  int n_wg;  // workgroups given to them
+  const void* src[kMaxSideCopies];
+  void* dst[kMaxSideCopies];
+  int64_t n16[kMaxSideCopies];  // 16-byte units of each copy
+};
+
 struct PartialArgs {
   const uint16_t* q;        // bf16 [B][Hq][128]
   const uint16_t* k;        // bf16 [num_blocks][Hkv][128/8][16][8]
@@ -42,6 +54,7 @@ struct PartialArgs {
   // (c * B + b) * out_hq + h - out_h0 of out / lse.  Final output: out_hq = Hq, out_h0 = 0;
   // workspace partials of a kv-head range hold only its heads: out_hq = ng * G, out_h0 = g0 * G.
   int out_hq, out_h0;
+  SideCopies copies;  // chunked launch only (the balanced launch takes none)
 };
 
 // Partial attention: one workgroup of `waves` wavefronts per (chunk, sequence, kv head).

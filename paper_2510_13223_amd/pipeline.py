@@ -7,14 +7,26 @@ channel stores the newly computed KV of layer i-1, so the per-layer transfer
 T_KV = S_kv * L * r / B hides under the per-layer compute when it is shorter.
 
 Here the compute stage of layer i is the split paged decode attention of that
-layer (``bana_decode_attn_fused`` over all partitions).  HIP streams at
-default priority carry the stages (compute, and one copy stream shared by
-fetches and stores unless asked for two); events order them: attention of
-layer i waits for the fetch of layer i's prefix blocks, a device buffer is
-refilled only after the store that last read it.  Layers rotate through a
-ring of device pools.  Orchestration only: transfers between pinned host
-memory and device memory are the library's stream-ordered copy kernel
-(``bana_copy_async``), the arithmetic is the library's attention kernel.
+layer (``bana_decode_attn_fused`` over all partitions).  Layers rotate through
+a ring of three device pools.  Two overlapped schedules:
+
+* ``run_fused``: one launch per layer on one stream.  The attention launch of
+  layer i carries the fetch of layer i+1 and the store of layer i-1 as side
+  copies in workgroups of its own (``bana_decode_attn_fused_copies``), so the
+  three stages overlap inside the launch and the stream alone orders them
+  against the neighbouring layers (the fetch into a ring slot follows, in an
+  earlier launch, the store that last read it).
+* ``run_pipelined``: three HIP streams at default priority (compute, and one
+  copy stream shared by fetches and stores unless asked for two) ordered by
+  events; transfers are the library's stream-ordered copy kernel
+  (``bana_copy_async``).  Each layer's attention waits on an event of the copy
+  stream, which costs a gap between consecutive attention launches.
+
+Every schedule runs the same launch plan (4 wavefronts per workgroup, chunked
+launch: the copy workgroups of the fused schedule need free CU slots beside a
+plan that would otherwise fill one dispatch round), so all give the same
+results bit for bit.  Orchestration only: the arithmetic and the copies are
+the library's kernels.
 """
 
 from __future__ import annotations
@@ -69,7 +81,8 @@ class LayerPipeline:
         B, Hq = w.batch, w.num_q_heads
         lens_all = (w.kv_end.astype(np.int64) - w.kv_begin).sum(axis=0)
         self.dims = bana.make_dims(B, Hq, w.num_kv_heads, w.max_blocks_per_seq, w.num_blocks,
-                                   max_range_tokens=int(lens_all.max()), total_range_tokens=int(lens_all.sum()))
+                                   max_range_tokens=int(lens_all.max()), total_range_tokens=int(lens_all.sum()),
+                                   nonempty_ranges=int(np.count_nonzero(lens_all)), waves_hint=4, plan_hint=1)
         ws = bana.bana_decode_attn_workspace_bytes(self.dims)
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=self.device) if ws else None
         self.out = torch.empty((self.L, B, Hq, bana.HEAD_DIM), dtype=torch.float32, device=self.device)
@@ -99,6 +112,27 @@ class LayerPipeline:
         self._fetch_bytes = fb * kb
         self._store_bytes = sb * kb
         self._kb = kb
+        # Side copies of each layer's launch in the fused schedule: fetch of layer i+1, store of i-1.
+        self._side = []
+        for i in range(self.L):
+            c = []
+            if i + 1 < self.L:
+                c += self._fetch_copies(i + 1)
+            if i >= 1:
+                c += self._store_copies(i - 1)
+            arr = (bana.bana_copy * max(1, len(c)))(*[bana.bana_copy(d, s_, n) for d, s_, n in c])
+            self._side.append((arr, len(c)))
+
+    def _fetch_copies(self, layer: int):
+        s = layer % self.ring
+        return [(self.pool_k[s].data_ptr(), self.host_fetch_k[layer].data_ptr(), self._fetch_bytes),
+                (self.pool_v[s].data_ptr(), self.host_fetch_v[layer].data_ptr(), self._fetch_bytes)]
+
+    def _store_copies(self, layer: int):
+        s = layer % self.ring
+        off = self.fb * self._kb
+        return [(self.host_store_k[layer].data_ptr(), self.pool_k[s].data_ptr() + off, self._store_bytes),
+                (self.host_store_v[layer].data_ptr(), self.pool_v[s].data_ptr() + off, self._store_bytes)]
 
     # -- stages ------------------------------------------------------------------------------------
     def _copy(self, dst: int, src: int, nbytes: int, stream) -> None:
@@ -111,9 +145,8 @@ class LayerPipeline:
             raise bana.BanaError(st, "bana_copy_async")
 
     def _fetch(self, layer: int, stream) -> None:
-        s = layer % self.ring
-        self._copy(self.pool_k[s].data_ptr(), self.host_fetch_k[layer].data_ptr(), self._fetch_bytes, stream)
-        self._copy(self.pool_v[s].data_ptr(), self.host_fetch_v[layer].data_ptr(), self._fetch_bytes, stream)
+        for dst, src, n in self._fetch_copies(layer):
+            self._copy(dst, src, n, stream)
 
     def _attend(self, layer: int, stream) -> None:
         st = bana.lib().bana_decode_attn_fused(*self._attn_args[layer], ctypes.c_void_p(stream.cuda_stream))
@@ -121,10 +154,15 @@ class LayerPipeline:
             raise bana.BanaError(st, "bana_decode_attn_fused")
 
     def _store(self, layer: int, stream) -> None:
-        s = layer % self.ring
-        off = self.fb * self._kb
-        self._copy(self.host_store_k[layer].data_ptr(), self.pool_k[s].data_ptr() + off, self._store_bytes, stream)
-        self._copy(self.host_store_v[layer].data_ptr(), self.pool_v[s].data_ptr() + off, self._store_bytes, stream)
+        for dst, src, n in self._store_copies(layer):
+            self._copy(dst, src, n, stream)
+
+    def _attend_with_copies(self, layer: int, stream) -> None:
+        arr, n = self._side[layer]
+        st = bana.lib().bana_decode_attn_fused_copies(*self._attn_args[layer], arr, n,
+                                                      ctypes.c_void_p(stream.cuda_stream))
+        if st != bana.BANA_OK:
+            raise bana.BanaError(st, "bana_decode_attn_fused_copies")
 
     # -- schedules ---------------------------------------------------------------------------------
     def run_serial(self) -> None:
@@ -134,6 +172,26 @@ class LayerPipeline:
             self._fetch(i, st)
             self._attend(i, st)
             self._store(i, st)
+
+    def run_fused(self, marks=None) -> None:
+        """One launch per layer on the compute stream: the attention of layer i with the fetch of
+        layer i+1 and the store of layer i-1 as side copies of the same launch.  The fetch of the
+        first layer and the store of the last (the pipeline's fill and drain) are copy launches of
+        their own; ``marks`` (two events) are recorded around the layer launches."""
+        st = self.s_comp
+        self._fetch(0, st)
+        if marks is not None:
+            marks[0].record(st)
+        for i in range(self.L):
+            self._attend_with_copies(i, st)
+        if marks is not None:
+            marks[1].record(st)
+        self._store(self.L - 1, st)
+
+    def run_attention_only(self) -> None:
+        """The attention launches alone (no transfers), for comparison."""
+        for i in range(self.L):
+            self._attend(i, self.s_comp)
 
     def run_pipelined(self, timing: bool = False) -> None:
         """Fetch of layer i+1 and store of layer i-1 overlap the attention of layer i."""
@@ -216,7 +274,8 @@ def t_f_layer_ms(t_f_ms: float, hit_rate: float, layers: int) -> float:
 
 def measure(workload: str = "llama3_8b", layers: int = 8, fetch_tokens: int = 500, store_tokens: int = 500,
             reps: int = 5) -> dict:
-    """Per-layer times of the serial and the pipelined schedules, and the measured T_KV.
+    """Per-layer times of the serial, three-stream and fused schedules (the fused one also in steady
+    state, without the pipeline's fill and drain), of the attention alone, and the measured T_KV.
 
     Defaults follow the paper's worked example for the store (Sec. 4.2): a 1000-token request with a
     50 % prefix-cache hit fetches 500 tokens of KV per layer (S_kv = 4 KiB per token per layer for
@@ -242,6 +301,17 @@ def measure(workload: str = "llama3_8b", layers: int = 8, fetch_tokens: int = 50
 
     serial = timed(pipe.run_serial)
     pipelined = timed(pipe.run_pipelined)
+    fused = timed(pipe.run_fused)
+    alone = timed(pipe.run_attention_only)
+    # Steady state of the fused schedule: events around the layer launches only (the fill and
+    # drain copies outside), median over repetitions.
+    steady = []
+    for _ in range(reps):
+        marks = [torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+        pipe.run_fused(marks)
+        torch.cuda.synchronize()
+        steady.append(marks[0].elapsed_time(marks[1]) / layers)
+    fused_steady = float(np.median(steady))
     pipe.run_pipelined(timing=True)
     stage = pipe.stage_ms.mean(axis=0)
     s_kv = w.num_kv_heads * HEAD_DIM_BYTES_PER_TOKEN
@@ -254,6 +324,11 @@ def measure(workload: str = "llama3_8b", layers: int = 8, fetch_tokens: int = 50
         "fetch_bytes_per_layer": fetch_bytes,
         "ms_per_layer_serial": round(serial, 5),
         "ms_per_layer_pipelined": round(pipelined, 5),
+        "ms_per_layer_fused_copies": round(fused, 5),
+        "ms_per_layer_fused_copies_steady": round(fused_steady, 5),
+        "ms_per_layer_attention_alone": round(alone, 5),
+        "fused_over_attention_alone": round(fused / alone, 4),
+        "fused_steady_over_attention_alone": round(fused_steady / alone, 4),
         "stage_ms_fetch_attend_store": [round(float(x), 5) for x in stage],
         "t_kv_measured_ms": round(float(stage[0]), 5),
         "h2d_gbs": round(fetch_bytes / (float(stage[0]) / 1e3) / 1e9, 2),

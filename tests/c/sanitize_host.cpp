@@ -70,6 +70,12 @@ hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t) {
   REQUIRE(inside(a.q, (unsigned __int128)a.B * a.Hq * 128 * 2));
   REQUIRE(inside(a.table, (unsigned __int128)a.B * a.max_blocks * 4));
   REQUIRE(inside(a.begin, (unsigned __int128)a.n_parts * a.B * 4) && inside(a.end, (unsigned __int128)a.n_parts * a.B * 4));
+  REQUIRE(a.copies.n >= 0 && a.copies.n <= kMaxSideCopies && a.copies.n_wg >= 0 && a.copies.n_wg <= 64);
+  REQUIRE((a.copies.n == 0) == (a.copies.n_wg == 0));
+  REQUIRE(((uint64_t)a.nc * a.B * a.ng + a.copies.n_wg) * 64 * waves <= kMaxItems);
+  for (int i = 0; i < a.copies.n; ++i)
+    REQUIRE(a.copies.n16[i] > 0 && inside(a.copies.src[i], (unsigned __int128)a.copies.n16[i] * 16) &&
+            inside(a.copies.dst[i], (unsigned __int128)a.copies.n16[i] * 16));
   return hipSuccess;
 }
 
@@ -247,7 +253,7 @@ int main(int argc, char** argv) {
     const int32_t* i32 = nullptr;
     auto I = [&](int i) { return static_cast<const int32_t*>(fake(i)); };
     auto F = [&](int i) { return static_cast<float*>(fake(i)); };
-    bana_status st[9];
+    bana_status st[10];
     st[0] = bana_decode_attn_partial(&d, fake(0), fake(1), fake(2), I(3), I(4), I(5), I(6), F(7), F(8), wsp,
                                      ws_bytes, nullptr);
     st[1] = bana_decode_attn_fused(&d, fake(0), fake(1), fake(2), I(3), I(4), I(5), I(6), n_parts, F(9), F(10), wsp,
@@ -265,6 +271,18 @@ int main(int argc, char** argv) {
     st[7] = bana_debug_kv_rows(&d, I(3), I(5), I(6), static_cast<int64_t*>(fake(24)), nullptr);
     st[8] = bana_debug_gather_read(&d, fake(1), fake(2), I(3), I(5), I(6), n_parts,
                                    static_cast<uint32_t*>(fake(24)), nullptr);
+    // the fused call with side copies (fake host / device buffers of the given sizes)
+    bana_copy copies[9];
+    const int n_copies = (int)rnd(0, 9);
+    for (int i = 0; i < n_copies; ++i) {
+      copies[i].bytes = (size_t)rnd(0, 1 << 20) * 16;
+      copies[i].dst = fake(11 + 2 * (i % 4));
+      copies[i].src = fake(12 + 2 * (i % 4));
+      add_region(copies[i].dst, copies[i].bytes);
+      add_region(copies[i].src, copies[i].bytes);
+    }
+    st[9] = bana_decode_attn_fused_copies(&d, fake(0), fake(1), fake(2), I(3), I(4), I(5), I(6), n_parts, F(9),
+                                          F(10), wsp, ws_bytes, copies, n_copies, nullptr);
     (void)i32;
     for (bana_status s : st) {
       REQUIRE(valid_status(s));

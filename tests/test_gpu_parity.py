@@ -519,6 +519,16 @@ def test_layer_pipeline_matches_serial_and_oracle():
     po, pl = pipe.outputs()
     ps = pipe.stored()
     assert np.array_equal(so, po) and np.array_equal(sl, pl)
+    # one launch per layer, the transfers carried by the attention launches
+    for t in pipe.host_store_k + pipe.host_store_v:
+        t.zero_()
+    pipe.out.fill_(float("nan"))
+    pipe.run_fused()
+    fo, fl = pipe.outputs()
+    fs = pipe.stored()
+    assert np.array_equal(so, fo) and np.array_equal(sl, fl)
+    for layer in range(st.num_layers):
+        assert np.array_equal(fs[layer][0], ss[layer][0]) and np.array_equal(fs[layer][1], ss[layer][1])
     fb, sb = st.fetch_blocks, st.store_blocks
     for layer in range(st.num_layers):
         uo, ul = oracle.workload_unsplit(W.layer_view(st, layer))
@@ -1025,3 +1035,36 @@ def test_lds_race_check_build_bit_identical(name, plan):
         dst.append((dk, dv))
     assert torch.equal(dst[0][0].view(torch.int16), dst[1][0].view(torch.int16))
     assert torch.equal(dst[0][1].view(torch.int16), dst[1][1].view(torch.int16))
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama3_8b"])
+def test_fused_copies_equal_the_fused_call_and_copy_exactly(name):
+    """bana_decode_attn_fused_copies: the attention equals bana_decode_attn_fused with the chunked
+    launch bit for bit, and its side copies (pinned host -> device, device -> pinned host, device ->
+    device, ragged sizes, a zero-byte copy) arrive byte for byte."""
+    w = _workload(name)
+    dw = DeviceWorkload(w, plan_hint=1, waves_hint=4)
+    B, Hq = w.batch, w.num_q_heads
+    ref_o = torch.empty((B, Hq, 128), device="cuda")
+    ref_l = torch.empty((B, Hq), device="cuda")
+    bana.bana_decode_attn_fused(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin, dw.kv_end,
+                                ref_o, ref_l, workspace=dw.workspace, dims=dw.fused_dims)
+    g = torch.Generator().manual_seed(7)
+    host_src = torch.randint(-2**31, 2**31 - 1, (((3 << 20) + 48) // 4,), dtype=torch.int32, generator=g).pin_memory()
+    dev_src = torch.randint(-2**31, 2**31 - 1, (((1 << 20) + 16) // 4,), dtype=torch.int32, generator=g).cuda()
+    dev_dst = torch.zeros_like(host_src, device="cuda")
+    host_dst = torch.zeros_like(dev_src, device="cpu").pin_memory()
+    dev_dst2 = torch.zeros_like(dev_src)
+    empty = torch.empty(0, dtype=torch.int32, device="cuda")
+    o = torch.full((B, Hq, 128), float("nan"), device="cuda")
+    l = torch.full((B, Hq), float("nan"), device="cuda")
+    bana.bana_decode_attn_fused_copies(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin,
+                                       dw.kv_end, o, l, copies=[(dev_dst, host_src), (host_dst, dev_src),
+                                                                (dev_dst2, dev_src), (empty, empty)],
+                                       workspace=dw.workspace, dims=dw.fused_dims)
+    torch.cuda.synchronize()
+    assert torch.equal(o.view(torch.int32), ref_o.view(torch.int32))
+    assert torch.equal(l.view(torch.int32), ref_l.view(torch.int32))
+    assert torch.equal(dev_dst.cpu(), host_src)
+    assert torch.equal(host_dst, dev_src.cpu())
+    assert torch.equal(dev_dst2, dev_src)

@@ -330,3 +330,26 @@ def test_static_scratch_size_matches_the_header():
     text = open(HEADER).read()
     m = re.search(r"#define BANA_STATIC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
     assert m and int(m.group(1)) << int(m.group(2)) == bana.STATIC_SCRATCH_BYTES
+
+
+def test_fused_copies_rejects_bad_arguments(lib):
+    d = _dims()
+
+    def call(n_copies, copies=None, n_parts=2, dd=d):
+        arr = copies if copies is not None else (bana.bana_copy * 1)(bana.bana_copy(0x200000, 0x300000, 64))
+        return lib.bana_decode_attn_fused_copies(ctypes.byref(dd) if dd is not None else None, *[FAKE] * 7, n_parts,
+                                                 FAKE, FAKE, None, 0, arr, n_copies, None)
+
+    assert call(1, n_parts=0) == -1
+    assert call(-1) == -1
+    assert call(9, (bana.bana_copy * 9)()) == -2
+    assert call(1, dd=None) == -1
+    assert call(1, dd=_dims(head_dim=64)) == -2
+    assert lib.bana_decode_attn_fused_copies(ctypes.byref(d), *[FAKE] * 7, 2, FAKE, FAKE, None, 0, None, 1,
+                                             None) == -1
+    for bad in (bana.bana_copy(0, 0x300000, 64), bana.bana_copy(0x200000, 0, 64),
+                bana.bana_copy(0x200008, 0x300000, 64), bana.bana_copy(0x200000, 0x300004, 64),
+                bana.bana_copy(0x200000, 0x300000, 24)):
+        assert call(1, (bana.bana_copy * 1)(bad)) == -1
+    # a zero-byte copy is skipped, whatever its pointers; the call then fails only on n_parts
+    assert call(1, (bana.bana_copy * 1)(bana.bana_copy(0, 0, 0)), n_parts=0) == -1
