@@ -58,6 +58,9 @@ def _parse():
     ap.add_argument("--chunks", type=int, default=0, help="chunks-per-range hint (0 = library plan)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (for scaling HBM byte counters)")
+    ap.add_argument("--profile-regions", action="store_true",
+                    help="for profiler runs: each call type in a region of its own (K scrubbed repetitions), "
+                         "regions separated by sentinel launches; prints the region list instead of timings")
     return ap.parse_args()
 
 
@@ -94,7 +97,7 @@ def _partial_algorithmic_bytes(w, p):
 
 KERNEL_SOURCES = ("paper_2510_13223_amd/csrc/attn_partial.hip", "paper_2510_13223_amd/csrc/paged_addr.h",
                   "paper_2510_13223_amd/csrc/kernels.h", "paper_2510_13223_amd/csrc/bana_api.cpp")
-TRAFFIC_PROFILE = "profiles/partial_attn_llama3_8b_pmc.md"
+TRAFFIC_PROFILE = "profiles/hbm_bytes_{workload}.md"
 
 
 def _kernel_source_sha256() -> str:
@@ -114,7 +117,7 @@ def _measured_traffic(workload: str):
     kernel sources as they are now (sha256 over the kernel's source files);
     otherwise None.
     """
-    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), TRAFFIC_PROFILE)
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), TRAFFIC_PROFILE.format(workload=workload))
     try:
         fields = {}
         for line in open(path):
@@ -180,6 +183,72 @@ def _cpu_baseline(w, target_s):
     }
 
 
+SENTINEL_BYTES = 4096  # sentinel launch: bana_debug_stream_read of 4 KiB by (region + 1) workgroups
+
+
+def _profile_regions(args, w, dw, stream, h, torch, bana, workloads):
+    """Profiler mode: every call type of the step (each partition's partial call, the merge, the
+    fused call, the migration of the last partition, each head half, the gather read) runs K times
+    in a region of its own, each repetition after a cache scrub (512 MiB written, then read back by
+    2048 workgroups), regions separated by a sentinel launch of bana_debug_stream_read over 4 KiB
+    with region + 1 workgroups, so a profiler's dispatch list splits into regions by kernel name
+    and grid size alone.  Prints one JSON line naming the regions in order."""
+    import numpy as np
+
+    dev = dw.q.device
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    scrub_sink = torch.empty(2048, dtype=torch.int32, device=dev)
+    sent_buf = torch.zeros(SENTINEL_BYTES, dtype=torch.uint8, device=dev)
+    regions = [(f"partition {p}", (lambda p=p: dw.partial(p, h))) for p in range(w.n_parts)]
+    regions += [("merge", lambda: dw.merge(h)), ("fused", lambda: dw.fused(h))]
+    mig = workloads.make_migration(w, w.n_parts - 1, seed=1)
+    to_dev = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+    d_k, d_v = to_dev(mig.dst_k), to_dev(mig.dst_v)
+    d_t, m_b, m_e = (torch.from_numpy(x).to(dev) for x in (mig.dst_table, mig.blk_begin, mig.blk_end))
+    hint = int(np.max(mig.blk_end - mig.blk_begin)) * 16
+    regions.append(("migration", lambda: bana.bana_migrate_kv_blocks(
+        dw.k_cache, dw.v_cache, dw.block_table, d_k, d_v, d_t, m_b, m_e, stream=stream, max_range_tokens=hint)))
+    lens = w.seq_lens.astype(np.int64)
+    hs_dims = bana.make_dims(w.batch, w.num_q_heads, w.num_kv_heads, w.max_blocks_per_seq, w.num_blocks,
+                             max_range_tokens=int(lens.max()), total_range_tokens=int(lens.sum()),
+                             nonempty_ranges=int(np.count_nonzero(lens)))
+    zeros = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+    hs_out = torch.empty((w.batch, w.num_q_heads, 128), dtype=torch.float32, device=dev)
+    hs_lse = torch.empty((w.batch, w.num_q_heads), dtype=torch.float32, device=dev)
+    half = max(1, w.num_kv_heads // 2)
+    for g0, g1 in ((0, half), (half, w.num_kv_heads)):
+        if g0 == g1:
+            continue
+        n = bana.bana_decode_attn_workspace_bytes(bana.head_range_dims(hs_dims, g0, g1))
+        ws = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)
+        regions.append((f"heads {g0}-{g1}", (lambda g0=g0, g1=g1, ws=ws: bana.bana_decode_attn_heads(
+            dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, zeros, dw.seq_lens, g0, g1, hs_out, hs_lse,
+            workspace=ws, stream=stream, dims=hs_dims))))
+    sink = torch.empty((w.batch, w.num_kv_heads), dtype=torch.int32, device=dev)
+    regions.append(("gather read", lambda: bana.bana_debug_gather_read(
+        dw.k_cache, dw.v_cache, dw.block_table, dw.kv_begin, dw.kv_end, sink, stream=stream)))
+    with torch.cuda.stream(stream):
+        for i, (name, fn) in enumerate(regions):
+            bana.bana_debug_stream_read(sent_buf, scrub_sink[:i + 1], stream=stream)
+            for k in range(args.steps):
+                scrub.fill_(k & 0xFF)
+                bana.bana_debug_stream_read(scrub, scrub_sink, stream=stream)
+                fn()
+            stream.synchronize()
+            print(f"[bench] region {i}: {name}", file=sys.stderr, flush=True)
+        bana.bana_debug_stream_read(sent_buf, scrub_sink[:len(regions) + 1], stream=stream)
+    if args.copy_calibration:
+        n = 1 << 30
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"metric": METRIC, "profile_regions": [r[0] for r in regions], "steps": args.steps,
+                      "config": _workload_desc(w), "copy_calibration_bytes": (1 << 30) if args.copy_calibration
+                      else 0}), flush=True)
+
+
 def main():
     args = _parse()
     if args.gpus != 1:
@@ -214,6 +283,10 @@ def main():
     P = w.n_parts
     h = ctypes.c_void_p(stream.cuda_stream)
     from paper_2510_13223_amd import bana
+
+    if args.profile_regions:
+        _profile_regions(args, w, dw, stream, h, torch, bana, workloads)
+        return
 
     # Every timed figure below is taken the same way: HIP events recorded on the stream the work
     # runs on, around each repetition alone, with a cache scrub between repetitions (outside the
