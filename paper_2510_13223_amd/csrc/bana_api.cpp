@@ -269,7 +269,6 @@ bana_status run_attention(const bana_dims* d, const void* q, const void* k_cache
   bana_dims sub = *d;
   sub.num_kv_heads = ng;
   sub.num_q_heads = ng * G;
-  if (side != nullptr && side->n > 0) sub.plan_hint = 1;  // side copies ride on the chunked launch
   Plan plan = make_plan(&sub);
   const WorkspaceLayout ws = layout_for(&sub, plan);
   if (ws.total > 0 && (workspace == nullptr || workspace_bytes < ws.total)) {
@@ -458,7 +457,10 @@ bana_status bana_decode_attn_fused_copies(const bana_dims* d, const void* q, con
     side.n16[side.n] = (int64_t)(c.bytes / 16);
     ++side.n;
   }
-  return run_attention(d, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts, 0,
+  // The side copies ride on the chunked launch, with or without bytes to move.
+  bana_dims chunked = *d;
+  chunked.plan_hint = 1;
+  return run_attention(&chunked, q, k_cache, v_cache, block_table, kv_range_begin, kv_range_end, n_parts, 0,
                        d->num_kv_heads, out, lse_out, workspace, workspace_bytes, stream, &side);
 }
 
