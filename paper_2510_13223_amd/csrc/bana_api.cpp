@@ -141,13 +141,16 @@ Plan make_plan(const bana_dims* d) {
   }
   if (p.balanced) {
     // Pieces of the row with the most: its blocks over intervals of at least s_lo blocks, plus
-    // the two partly covered intervals at its ends.  Many pieces per row, or few rows (long
-    // sequences of a small batch), spread each row's pieces over several thread groups.
+    // the two partly covered intervals at its ends.  Few rows (long sequences of a small batch)
+    // spread each row's pieces over 8 thread groups; with many rows, one group per row streams
+    // best unless a row has very many pieces (measured on MI355X, cold caches: mixed's migrated
+    // partition, 8,192 rows, 68 / 69 / 71 / 76 us with 1 / 2 / 4 / 8 groups; long's partitions,
+    // 256 rows, fastest with 8).
     const int64_t u_lo = hinted ? std::max<int64_t>(1, d->total_range_tokens / kBlockSize) : 1;
     const int64_t s_lo = std::max<int64_t>(1, u_lo / p.K);
     const int64_t pieces = (bound + 1) / s_lo + 2;
     const int64_t rows = (int64_t)d->batch * d->num_q_heads;
-    p.kp = pieces >= 32 || rows < 4096 ? 8 : pieces >= 16 ? 4 : pieces >= 8 ? 2 : 1;
+    p.kp = rows < 4096 ? 8 : pieces >= 64 ? 2 : 1;
   }
   if (p.balanced) {
     p.waves = bana::kBalancedWaves;

@@ -81,8 +81,6 @@ __global__ __launch_bounds__(256) void merge_few_kernel(const float* __restrict_
   if (lse_out != nullptr && d4 == 0) lse_out[orow] = M + logf(wsum);
 }
 
-constexpr int kUnroll = 4;  // partial rows per round (two rounds in flight per lane)
-
 // Any number of parts.  Group k (of KP) of a row takes parts k, k + KP, ...;
 // its q-th part is p = k + KP q.  Part p of merged row r (head i of sequence
 // b) is row base + p * prow of the part buffers: base = b * in_hq + in_h0 + i
@@ -91,7 +89,12 @@ constexpr int kUnroll = 4;  // partial rows per round (two rounds in flight per 
 // and prow = in_hq (the slots of a sequence's pieces are consecutive), and the
 // part count comes from the block-count prefix sums (pieces = intervals of S
 // blocks that overlap the sequence's blocks [prefix[b], prefix[b + 1])).
-template <int KP, bool PIECES>
+//
+// Rows stream in rounds of U parts (two rounds in flight per lane).  The many-part merge of many
+// rows takes one part per round: with fewer part streams in flight per wavefront the 16-part
+// merge of 32,768 rows runs in 50 us instead of 57 (U = 4) or 62 (U = 8) on MI355X, cold caches;
+// the piece merges, few pieces per row, keep U = 4 (U = 1 costs them 2 us).
+template <int KP, bool PIECES, int U>
 __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict__ outs,
                                                          const float* __restrict__ lses, int n_parts, MergeRows mr,
                                                          float* __restrict__ out, float* __restrict__ lse_out,
@@ -116,8 +119,8 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
     n = 0;
     prow = mr.in_hq;
     if (live) {
-      const int p0 = prefix[b], p1 = prefix[b + 1], U = prefix[mr.B];
-      const int64_t S = U > K ? ((int64_t)U + K - 1) / K : 1;
+      const int p0 = prefix[b], p1 = prefix[b + 1], total = prefix[mr.B];
+      const int64_t S = total > K ? ((int64_t)total + K - 1) / K : 1;
       if (p1 > p0) {  // slots clamped to [b, K + b): prefix sums from another call cannot reach outside
         const int64_t first = min(max((int64_t)p0 / S, (int64_t)0), (int64_t)K - 1);
         const int64_t last = min(max((int64_t)(p1 - 1) / S, first), (int64_t)K - 1);
@@ -134,13 +137,13 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
   // Group max: lane d4 reads parts q = d4, d4 + 32, ...  The first round of partial rows is
   // requested at the same time: rows do not depend on any lse (the weights reach them by
   // shuffle), so the group waits on one round of memory latency for both.  Then the rows stream
-  // in rounds of kUnroll, the next round requested before the current one is summed.  Rows of
+  // in rounds of U, the next round requested before the current one is summed.  Rows of
   // empty parts are loaded too (they lie inside the part buffer) but never enter a sum.
   float l0 = -INFINITY;
   if (d4 < nq) l0 = lrow[d4 * lstride];
-  f32x4 o[kUnroll];
+  f32x4 o[U];
 #pragma unroll
-  for (int u = 0; u < kUnroll; ++u)
+  for (int u = 0; u < U; ++u)
     if (u < nq) o[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(orow + u * lstride * 128) + d4);
   float m = l0;
   for (int q = d4 + 32; q < nq; q += 32) m = fmaxf(m, lrow[q * lstride]);
@@ -154,21 +157,21 @@ __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict
     // and for empty parts).
     float wq = l0 == -INFINITY ? 0.f : expf(l0 - m);
 #pragma unroll 1
-    for (int q = 0; q < nq; q += kUnroll) {
+    for (int q = 0; q < nq; q += U) {
       if (q > 0 && (q & 31) == 0) {
         const float lq = q + d4 < nq ? lrow[(q + d4) * lstride] : -INFINITY;
         wq = lq == -INFINITY ? 0.f : expf(lq - m);
       }
-      f32x4 cur[kUnroll];
+      f32x4 cur[U];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) cur[u] = o[u];
+      for (int u = 0; u < U; ++u) cur[u] = o[u];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u)
-        if (q + kUnroll + u < nq)
+      for (int u = 0; u < U; ++u)
+        if (q + U + u < nq)
           o[u] = __builtin_nontemporal_load(
-              reinterpret_cast<const f32x4*>(orow + (q + kUnroll + u) * lstride * 128) + d4);
+              reinterpret_cast<const f32x4*>(orow + (q + U + u) * lstride * 128) + d4);
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
+      for (int u = 0; u < U; ++u) {
         if (q + u < nq) {
           const float w = __shfl(wq, (q + u) & 31, 32);
           wsum += w;
@@ -221,8 +224,9 @@ hipError_t launch_many(const float* outs, const float* lses, int n_parts, const 
   constexpr int R = 256 / (32 * KP);
   const int64_t rows = m.B * m.hn;
   const unsigned grid = (unsigned)((rows + R - 1) / R);
-  hipLaunchKernelGGL((merge_many_kernel<KP, PIECES>), dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, m, out,
-                     lse_out, prefix, K);
+  constexpr int U = KP == 1 && !PIECES ? 1 : 4;
+  hipLaunchKernelGGL((merge_many_kernel<KP, PIECES, U>), dim3(grid), dim3(256), 0, stream, outs, lses, n_parts, m,
+                     out, lse_out, prefix, K);
   return hipGetLastError();
 }
 
