@@ -391,6 +391,28 @@ bana_status bana_debug_gather_read(const bana_dims* d, const void* k_cache, cons
  */
 bana_status bana_debug_stream_read(const void* src, size_t bytes, int32_t n_groups, uint32_t* sink, void* stream);
 
+/*
+ * Measurement hook of the wavefront-timeline build (libbana_timeline.so, the
+ * library compiled with BANA_WAVE_TIMELINE; same kernels and results): lane 0
+ * of every wavefront of the attention launches (chunked and balanced) stores
+ * readings of the GPU's constant 100 MHz clock in slot
+ *   (workgroup index * wavefronts per workgroup + wavefront) mod BANA_TIMELINE_SLOTS
+ * of a device table: [0] entry, [1] schedule ready (its ranges read, or the
+ * balanced launch's prefix scan done), [2] first KV block consumed (the
+ * earliest over the wavefront's pieces), [3] exit.  Side-copy workgroups and
+ * wavefronts without work leave [2] (and those that exit early [3]) as they
+ * were.
+ * bana_debug_wave_timeline_clear: sets every slot word to UINT64_MAX after the
+ *   stream's earlier work; returns when done.
+ * bana_debug_wave_timeline_read: copies slots [0, n_slots) to out (host
+ *   memory, uint64 [n_slots][4]) after the stream's earlier work; returns when
+ *   done.  BANA_ERR_INVALID for a NULL out or n_slots > BANA_TIMELINE_SLOTS.
+ * The product library returns BANA_ERR_UNSUPPORTED from both.
+ */
+#define BANA_TIMELINE_SLOTS (1 << 18)
+bana_status bana_debug_wave_timeline_clear(void* stream);
+bana_status bana_debug_wave_timeline_read(uint64_t* out, size_t n_slots, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

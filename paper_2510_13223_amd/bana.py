@@ -18,6 +18,8 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("BANA_LIBRARY") or os.path.join(_PKG, "libbana.so")
 RACECHECK_LIB_PATH = os.path.join(_PKG, "libbana_racecheck.so")
+TIMELINE_LIB_PATH = os.path.join(_PKG, "libbana_timeline.so")
+TIMELINE_SLOTS = 1 << 18  # BANA_TIMELINE_SLOTS
 
 HEAD_DIM = 128
 BLOCK_SIZE = 16
@@ -111,6 +113,10 @@ def load(path: str) -> ctypes.CDLL:
     L.bana_debug_gather_read.restype = ctypes.c_int
     L.bana_debug_stream_read.argtypes = [P, ctypes.c_size_t, ctypes.c_int32, P, P]
     L.bana_debug_stream_read.restype = ctypes.c_int
+    L.bana_debug_wave_timeline_clear.argtypes = [P]
+    L.bana_debug_wave_timeline_clear.restype = ctypes.c_int
+    L.bana_debug_wave_timeline_read.argtypes = [P, ctypes.c_size_t, P]
+    L.bana_debug_wave_timeline_read.restype = ctypes.c_int
     return L
 
 
@@ -504,3 +510,27 @@ def bana_copy_async(dst: torch.Tensor, src: torch.Tensor, stream=None) -> None:
     st = lib().bana_copy_async(_ptr(dst), _ptr(src), nbytes, _stream(stream))
     if st != BANA_OK:
         raise BanaError(st, "bana_copy_async")
+
+
+def bana_debug_wave_timeline_clear(stream=None, library: Optional[ctypes.CDLL] = None) -> None:
+    """Reset the wavefront timeline of the timeline build (``library``, default the loaded one).
+
+    See ``bana_debug_wave_timeline_clear`` in include/bana.h; raises BanaError (BANA_ERR_UNSUPPORTED)
+    on the product build.
+    """
+    st = (library or lib()).bana_debug_wave_timeline_clear(_stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_debug_wave_timeline_clear")
+
+
+def bana_debug_wave_timeline_read(n_slots: int, stream=None, library: Optional[ctypes.CDLL] = None):
+    """Slots [0, n_slots) of the wavefront timeline as a uint64 numpy array [n_slots, 4] (clock ticks
+    of 10 ns: entry, schedule ready, first block, exit; UINT64_MAX where nothing was written)."""
+    import numpy as np
+
+    out = np.empty((n_slots, 4), dtype=np.uint64)
+    st = (library or lib()).bana_debug_wave_timeline_read(out.ctypes.data_as(ctypes.c_void_p), n_slots,
+                                                         _stream(stream))
+    if st != BANA_OK:
+        raise BanaError(st, "bana_debug_wave_timeline_read")
+    return out

@@ -71,6 +71,17 @@ def build_racecheck(verbose: bool = False) -> str:
     return build(verbose, out=RACECHECK_LIB, defines=("BANA_LDS_RACE_CHECK",))
 
 
+TIMELINE_LIB = os.path.join(PKG, "libbana_timeline.so")
+
+
+def build_timeline(verbose: bool = False) -> str:
+    """The wavefront-timeline build (BANA_WAVE_TIMELINE): every wavefront of the attention launches
+    records clock readings (entry, schedule ready, first block, exit) for bana_debug_wave_timeline_read;
+    a GPU test requires its results to equal the product build's."""
+    return build(verbose, out=TIMELINE_LIB, defines=("BANA_WAVE_TIMELINE",))
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
     print(build_racecheck(verbose="-v" in sys.argv))
+    print(build_timeline(verbose="-v" in sys.argv))

@@ -78,6 +78,32 @@ constexpr int kRowPad = kHeadDim + 4;     // LDS row stride (floats) for the com
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Wavefront timeline (a measurement build only, BANA_WAVE_TIMELINE): lane 0 of every wavefront of
+// the attention launches stores readings of the constant 100 MHz clock in its slot
+// (workgroup * wavefronts per workgroup + wavefront, modulo the table): entry, schedule ready,
+// first block consumed (the earliest over its pieces), exit.  The product build compiles the
+// marks away.
+#ifdef BANA_WAVE_TIMELINE
+__device__ unsigned long long g_wave_timeline[(size_t)BANA_TIMELINE_SLOTS * 4];
+__device__ __forceinline__ unsigned long long* timeline_slot() {
+  const unsigned slot = (blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) % BANA_TIMELINE_SLOTS;
+  return g_wave_timeline + (size_t)slot * 4;
+}
+#define BANA_TIMELINE_MARK(i)                                                      \
+  do {                                                                             \
+    const unsigned long long t_ = __builtin_amdgcn_s_memrealtime();                \
+    if ((threadIdx.x & 63) == 0) timeline_slot()[i] = t_;                          \
+  } while (0)
+#define BANA_TIMELINE_FIRST()                                                      \
+  do {                                                                             \
+    const unsigned long long t_ = __builtin_amdgcn_s_memrealtime();                \
+    if ((threadIdx.x & 63) == 0) atomicMin(timeline_slot() + 2, t_);               \
+  } while (0)
+#else
+#define BANA_TIMELINE_MARK(i) ((void)0)
+#define BANA_TIMELINE_FIRST() ((void)0)
+#endif
+
 // Max over the 4 lanes of a column (lanes l, l^16, l^32, l^48).
 __device__ __forceinline__ float column_max(float x) {
   x = fmaxf(x, __shfl_xor(x, 16));
@@ -302,12 +328,14 @@ __device__ __forceinline__ void walk_blocks(Online& st, const bf16x8 (&qop)[4], 
     load_k(kr, a.k, tile_next, col, quad);
     seek(sg, cm, jr, n_parts);
     st.update(s, vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1, quad);
+    BANA_TIMELINE_FIRST();
     load_v(vr, a.v, tile_next, col, quad);
     jr += STEP;
     blk_next = blk_after;
   }
   seek(sg, cm, jr, n_parts);
   st.update(block_scores(qop, kr), vr, cm.jfirst + (jr - cm.vstart), cm.t0, cm.t1, quad);
+  BANA_TIMELINE_FIRST();
 }
 
 // Side copies: copy k is moved by the copy workgroups wg with wg % n == k, so all copies (host to
@@ -354,6 +382,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     side_copy(a.copies, blockIdx.x, threadIdx.x, 64 * W);
     return;
   }
+  BANA_TIMELINE_MARK(0);
   int wg = blockIdx.x - a.copies.n_wg;
   const int g = a.g0 + wg % a.ng;
   wg /= a.ng;
@@ -366,6 +395,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   Segments sg;
   sg.load(a, b, lane, n_parts);
   const int nblk = sg.total(n_parts);
+  BANA_TIMELINE_MARK(1);
   int per = (nblk + a.nc - 1) / a.nc;
   if (per < a.cmin) per = a.cmin;
   const int nch = nblk > 0 ? (nblk + per - 1) / per : 0;
@@ -394,6 +424,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
 
   if (W == 1) {
     st.emit(out_dst, lse_dst, col, quad, G);
+    BANA_TIMELINE_MARK(3);
     return;
   }
 
@@ -432,6 +463,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     *reinterpret_cast<f32x4*>(out_dst + h * kHeadDim + 4 * d4) = o * (1.0f / L);
     if (d4 == 0) lse_dst[h] = M + logf(L);
   }
+  BANA_TIMELINE_MARK(3);
 }
 
 // Balanced launch: wavefront k of kv head g walks the blocks [k S, (k + 1) S)
@@ -447,6 +479,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
 template <int W>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) void balanced_attn_kernel(
     PartialArgs a, int32_t* __restrict__ prefix, int K) {
+  BANA_TIMELINE_MARK(0);
   constexpr int kThreads = 64 * W;
   constexpr int kPerThread = (kMaxBalancedBatch + kThreads - 1) / kThreads;
   __shared__ int32_t sm_incl[kMaxBalancedBatch];
@@ -502,6 +535,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
   if (blockIdx.x == 0) {
     for (int i = threadIdx.x; i <= B; i += kThreads) prefix[i] = i == 0 ? 0 : sm_incl[i - 1];
   }
+  BANA_TIMELINE_MARK(1);
   const int g = a.g0 + (int)(blockIdx.x % (unsigned)a.ng);
   const int k = (int)(blockIdx.x / (unsigned)a.ng) * W + wave;
   if (k >= K) return;
@@ -537,6 +571,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(4, 8))) 
     st.emit(a.out + row0 * kHeadDim, a.lse + row0, col, quad, G);
     pos = pb + v1;
   }
+  BANA_TIMELINE_MARK(3);
 }
 
 }  // namespace
@@ -565,6 +600,34 @@ hipError_t launch_partial_attn(const PartialArgs& a, int waves, hipStream_t stre
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+hipError_t timeline_clear(hipStream_t stream) {
+#ifdef BANA_WAVE_TIMELINE
+  void* p = nullptr;
+  hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(g_wave_timeline));
+  if (e == hipSuccess) e = hipMemsetAsync(p, 0xFF, sizeof(g_wave_timeline), stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  return e;
+#else
+  (void)stream;
+  return hipErrorNotSupported;
+#endif
+}
+
+hipError_t timeline_read(uint64_t* out, size_t n_slots, hipStream_t stream) {
+#ifdef BANA_WAVE_TIMELINE
+  void* p = nullptr;
+  hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(g_wave_timeline));
+  if (e == hipSuccess) e = hipMemcpyAsync(out, p, n_slots * 4 * sizeof(uint64_t), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  return e;
+#else
+  (void)out;
+  (void)n_slots;
+  (void)stream;
+  return hipErrorNotSupported;
+#endif
 }
 
 hipError_t launch_balanced_attn(const PartialArgs& a, int32_t* prefix, int K, hipStream_t stream) {

@@ -563,6 +563,19 @@ bana_status bana_debug_gather_read(const bana_dims* d, const void* k_cache, cons
                                                 static_cast<hipStream_t>(stream)));
 }
 
+bana_status bana_debug_wave_timeline_clear(void* stream) {
+  const hipError_t e = bana::timeline_clear(static_cast<hipStream_t>(stream));
+  if (e == hipErrorNotSupported) return BANA_ERR_UNSUPPORTED;
+  return device_status(e);
+}
+
+bana_status bana_debug_wave_timeline_read(uint64_t* out, size_t n_slots, void* stream) {
+  if (!out || n_slots > (size_t)BANA_TIMELINE_SLOTS) return BANA_ERR_INVALID;
+  const hipError_t e = bana::timeline_read(out, n_slots, static_cast<hipStream_t>(stream));
+  if (e == hipErrorNotSupported) return BANA_ERR_UNSUPPORTED;
+  return device_status(e);
+}
+
 bana_status bana_debug_stream_read(const void* src, size_t bytes, int32_t n_groups, uint32_t* sink, void* stream) {
   if (!src || !sink || bytes % 16 != 0 || !aligned16(src) || n_groups < 1 || n_groups > 65536)
     return BANA_ERR_INVALID;

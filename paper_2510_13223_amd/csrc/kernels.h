@@ -23,6 +23,12 @@ __device__ __forceinline__ void race_check_delay(int) {}
 __device__ __forceinline__ void race_check_barrier() {}
 #endif
 
+// Wavefront timeline of the measurement build (BANA_WAVE_TIMELINE): set every slot to UINT64_MAX /
+// copy the first n_slots slots (uint64 [n_slots][4]) to host memory, both after the stream's
+// earlier work and synchronous with the host.  hipErrorNotSupported in the product build.
+hipError_t timeline_clear(hipStream_t stream);
+hipError_t timeline_read(uint64_t* out, size_t n_slots, hipStream_t stream);
+
 // Host <-> device copies carried by extra workgroups of an attention launch: they take the
 // launch's first n_wg workgroups, so they are dispatched before the attention's and run beside
 // them (the layer-wise pipeline's fetch and store, inside the attention launch of a layer).

@@ -166,6 +166,10 @@ hipError_t launch_debug_rows(const int32_t* table, const int32_t* begin, const i
   return hipSuccess;
 }
 
+// The product build's timeline hooks: nothing recorded.
+hipError_t timeline_clear(hipStream_t) { return hipErrorNotSupported; }
+hipError_t timeline_read(uint64_t*, size_t, hipStream_t) { return hipErrorNotSupported; }
+
 hipError_t static_scratch(void** ptr) {
   *ptr = reinterpret_cast<void*>(uintptr_t{40} << 44);  // apart from every fake buffer below
   add_region(*ptr, kStaticScratchBytes);

@@ -325,8 +325,10 @@ def test_fused_dominant_key_and_all_empty():
 
 # (parts, batch, heads): the few-part kernel, and the many-part kernel with 1, 2, 4 and 8 thread
 # groups per row, including more than 32 parts per group (several lse rounds per lane).
+# Many rows take one thread group per row, streaming one part per round: up to 32 parts (one lse
+# round per lane), more than 32, and a row count that leaves the last workgroup partly filled.
 @pytest.mark.parametrize("n,B,Hq", [(2, 7, 8), (4, 3, 8), (5, 7, 8), (9, 7, 8), (20, 3, 8), (70, 2, 8),
-                                    (300, 2, 8), (40, 128, 32), (6, 1, 1)])
+                                    (300, 2, 8), (40, 128, 32), (6, 1, 1), (16, 128, 32), (12, 4099, 1)])
 def test_merge_matches_oracle_merge(n, B, Hq):
     rng = np.random.default_rng(n * 1000 + B)
     outs = rng.standard_normal((n, B, Hq, 128)).astype(np.float32)
@@ -927,6 +929,20 @@ def test_random_shapes_many_sequences(case):
         _full_parity(w, plan_hint=plan)
 
 
+def test_balanced_piece_merge_many_rows_many_pieces():
+    """A balanced launch over 5,120 merged rows in which one sequence spans ~170 intervals (the piece
+    merge with two thread groups per row) and the rest fit in one or two, against the oracle."""
+    rng = np.random.default_rng(4242)
+    B = 160
+    lens = [int(x) for x in rng.integers(1, 65, size=B)]
+    lens[37] = 8000
+    cuts = [L // 3 if b == 37 else int(rng.integers(0, L + 1)) for b, L in enumerate(lens)]
+    ranges = [[(0, c) for c in cuts], [(c, L) for c, L in zip(cuts, lens)]]
+    w = W.make_custom(4242, B, 32, 8, lens, ranges, q_scale=1 / math.sqrt(128))
+    for plan in (2, 0):
+        _full_parity(w, plan_hint=plan)
+
+
 @pytest.mark.parametrize("B", [2048, 2049])
 def test_balanced_launch_at_its_batch_limit(B):
     """2048 sequences (the balanced schedule's limit: four per thread of the LDS scan) run the
@@ -1035,6 +1051,44 @@ def test_lds_race_check_build_bit_identical(name, plan):
         dst.append((dk, dv))
     assert torch.equal(dst[0][0].view(torch.int16), dst[1][0].view(torch.int16))
     assert torch.equal(dst[0][1].view(torch.int16), dst[1][1].view(torch.int16))
+
+
+@pytest.mark.parametrize("name,plan", [("tiny", 0), ("tiny", 2), ("mixed", 0)])
+def test_wave_timeline_build_bit_identical_and_ordered(name, plan):
+    """The wavefront-timeline build gives the product build's results bit for bit (chunked launch;
+    balanced launch with its piece merge; mixed's four dispatch rounds and its balanced migrated
+    partition), and its clock readings are ordered: entry <= schedule ready <= first block <= exit
+    for every wavefront of the last call that recorded them."""
+    from paper_2510_13223_amd import timeline
+
+    side = bana.load(bana.TIMELINE_LIB_PATH)
+    w = _workload(name)
+    dw = DeviceWorkload(w, plan_hint=plan)
+    h = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    outs = (dw.out_partials, dw.lses, dw.out, dw.lse_out, dw.fused_out, dw.fused_lse)
+    _raw_step(bana.lib(), dw, h)
+    ref = [t.clone() for t in outs]
+    for t in outs:
+        t.fill_(float("nan"))
+    _raw_step(side, dw, h)
+    torch.cuda.synchronize()
+    for a, b in zip(outs, ref):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    for p in range(w.n_parts):
+        bana.bana_debug_wave_timeline_clear(library=side)
+        assert side.bana_decode_attn_partial(*dw._partial_args[p], h) == bana.BANA_OK
+        t = bana.bana_debug_wave_timeline_read(bana.TIMELINE_SLOTS, library=side)
+        used = t[:, 0] != timeline.UNSET
+        assert used.sum() > 0
+        t = t[used]
+        assert np.all(t[:, 1] != timeline.UNSET) and np.all(t[:, 0] <= t[:, 1])
+        done = t[:, 3] != timeline.UNSET
+        assert done.sum() > 0 and np.all(t[done, 1] <= t[done, 3])
+        first = t[:, 2] != timeline.UNSET
+        assert first.sum() > 0 and np.all(t[first, 1] <= t[first, 2])
+        assert np.all(t[first & done, 2] <= t[first & done, 3])
+        s = timeline.summarize(t)
+        assert s["waves"] == len(t) and 0 < s["span_us"] < 1e5
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama3_8b"])

@@ -353,3 +353,21 @@ def test_fused_copies_rejects_bad_arguments(lib):
         assert call(1, (bana.bana_copy * 1)(bad)) == -1
     # a zero-byte copy is skipped, whatever its pointers; the call then fails only on n_parts
     assert call(1, (bana.bana_copy * 1)(bana.bana_copy(0, 0, 0)), n_parts=0) == -1
+
+
+def test_wave_timeline_hooks_are_unsupported_in_the_product_build(lib):
+    """The timeline entry points exist in every build; only the measurement build
+    (libbana_timeline.so) implements them.  The product build refuses before any HIP call."""
+    import numpy as np
+
+    out = np.zeros((4, 4), dtype=np.uint64)
+    assert lib.bana_debug_wave_timeline_clear(None) == bana.BANA_ERR_UNSUPPORTED
+    assert lib.bana_debug_wave_timeline_read(out.ctypes.data_as(ctypes.c_void_p), 4, None) == bana.BANA_ERR_UNSUPPORTED
+    assert lib.bana_debug_wave_timeline_read(None, 4, None) == bana.BANA_ERR_INVALID
+    assert lib.bana_debug_wave_timeline_read(out.ctypes.data_as(ctypes.c_void_p), bana.TIMELINE_SLOTS + 1,
+                                             None) == bana.BANA_ERR_INVALID
+    with pytest.raises(bana.BanaError):
+        bana.bana_debug_wave_timeline_read(4, stream=0)
+    # the header's slot count and the binding's agree
+    text = open(HEADER).read()
+    assert re.search(r"#define BANA_TIMELINE_SLOTS \(1 << 18\)", text) and bana.TIMELINE_SLOTS == 1 << 18
