@@ -90,10 +90,12 @@ __global__ __launch_bounds__(256) void merge_few_kernel(const float* __restrict_
 // part count comes from the block-count prefix sums (pieces = intervals of S
 // blocks that overlap the sequence's blocks [prefix[b], prefix[b + 1])).
 //
-// Rows stream in rounds of U parts (two rounds in flight per lane).  The many-part merge of many
-// rows takes one part per round: with fewer part streams in flight per wavefront the 16-part
-// merge of 32,768 rows runs in 50 us instead of 57 (U = 4) or 62 (U = 8) on MI355X, cold caches;
-// the piece merges, few pieces per row, keep U = 4 (U = 1 costs them 2 us).
+// Rows stream in rounds of U parts, each round requested before the previous one is summed (the
+// waits the compiler places keep about one round in flight per lane, its loads overlapping the
+// sums of the round before).  The many-part merge of many rows takes one part per round: with fewer
+// part streams in flight per wavefront the 16-part merge of 32,768 rows runs in 50 us instead of
+// 57 (U = 4) or 62 (U = 8) on MI355X, cold caches; the piece merges, few pieces per row, keep
+// U = 4 (U = 1 costs them 2 us).
 template <int KP, bool PIECES, int U>
 __global__ __launch_bounds__(256) void merge_many_kernel(const float* __restrict__ outs,
                                                          const float* __restrict__ lses, int n_parts, MergeRows mr,
