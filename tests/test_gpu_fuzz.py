@@ -1,0 +1,96 @@
+"""Seeded random-shape fuzz of the partial, merge and fused calls against the fp64 oracle (GPU).
+
+Each case draws a workload shape (1-400 sequences, GQA groups 1-16, 1-6 ranges per sequence, some
+sequences with overlapping or gapped ranges), lengths from one of four mixes (many short; few long;
+log-normal with a heavy tail; one long among many tiny) and random launch hints (waves, chunks, plan,
+dispatch order, no workspace, no range hints), runs every partition's call, the merge and the fused
+call, and checks them against the oracle's partials and their merge (which, unlike unsplit
+attention, also covers overlapping ranges).  By default a few cases run; ``BANA_FUZZ_SECONDS=<s>``
+runs cases for that long instead (``BANA_FUZZ_SEED`` picks the stream).
+"""
+
+import math
+import os
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2510_13223_amd import workloads as W
+from paper_2510_13223_amd.runner import DeviceWorkload
+
+from test_gpu_parity import _check_lse, _check_out, _log
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(seed, case):
+    rng = np.random.default_rng(777000 + seed * 100000 + case)
+    kind = int(rng.integers(0, 4))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    Hq = Hkv * int(rng.choice([1, 2, 3, 4, 5, 8, 16]))
+    n_parts = int(rng.integers(1, 7))
+    if kind == 0:  # many short sequences
+        B = int(rng.integers(1, 400))
+        lens = rng.integers(1, 300, size=B)
+    elif kind == 1:  # few long ones
+        B = int(rng.integers(1, 6))
+        lens = rng.integers(1, 20000, size=B)
+    elif kind == 2:  # log-normal with a heavy tail
+        B = int(rng.integers(2, 200))
+        lens = np.clip(np.rint(np.exp(rng.normal(np.log(200), 1.3, size=B))), 1, 12000)
+    else:  # one long among many tiny
+        B = int(rng.integers(2, 300))
+        lens = rng.integers(1, 40, size=B)
+        lens[int(rng.integers(0, B))] = int(rng.integers(2000, 16000))
+    lens = [int(x) for x in lens]
+    ranges = [[] for _ in range(n_parts)]
+    for L in lens:
+        if rng.random() < 0.15:  # independent ranges: overlapping or leaving gaps
+            for p in range(n_parts):
+                a = int(rng.integers(0, L + 1))
+                ranges[p].append((a, int(rng.integers(a, L + 1))))
+        else:
+            cuts = np.sort(rng.integers(0, L + 1, size=n_parts - 1)).tolist()
+            edges = [0] + cuts + [L]
+            for p in range(n_parts):
+                ranges[p].append((edges[p], edges[p + 1]))
+    kw = dict(waves_hint=int(rng.choice([0, 0, 0, 1, 2, 4, 8])), chunks_hint=int(rng.choice([0, 0, 0, 1, 2, 3, 7])),
+              plan_hint=int(rng.choice([0, 0, 1, 2])), order_hints=bool(rng.integers(0, 2)),
+              use_workspace=bool(rng.integers(0, 5) > 0), range_hints=bool(rng.integers(0, 5) > 0))
+    w = W.make_custom(880000 + case, B, Hq, Hkv, lens, ranges, q_scale=1 / math.sqrt(128))
+    return w, kw, f"fuzz {seed}:{case} kind={kind} B={B} Hq={Hq} Hkv={Hkv} parts={n_parts} maxL={max(lens)} {kw}"
+
+
+def _check(w, kw):
+    dw = DeviceWorkload(w, **kw)
+    op, lp, out, lse_out = dw.results()
+    ro, rl = oracle.workload_partials(w)
+    for p in range(w.n_parts):
+        _check_out(op[p][np.isfinite(rl[p])], ro[p][np.isfinite(rl[p])], f"part {p} out_partial")
+        assert np.all(op[p][np.isneginf(rl[p])] == 0.0), "empty partition must give out_partial = 0"
+        _check_lse(lp[p], rl[p], f"part {p}")
+    mo, ml = oracle.merge(ro, rl)
+    fin = np.isfinite(ml)
+    _check_out(out[fin], mo[fin], "merged out")
+    assert np.all(out[~fin] == 0.0)
+    _check_lse(lse_out, ml, "merged lse")
+    fo, fl = dw.fused_results()
+    _check_out(fo[fin], mo[fin], "fused out")
+    _check_lse(fl, ml, "fused lse")
+
+
+def test_random_shape_fuzz():
+    seed = int(os.environ.get("BANA_FUZZ_SEED", "0"))
+    seconds = float(os.environ.get("BANA_FUZZ_SECONDS", "0"))
+    t_end = time.time() + seconds
+    case = 0
+    while case < 16 or time.time() < t_end:
+        w, kw, tag = _case(seed, case)
+        _log(tag)
+        _check(w, kw)
+        torch.cuda.empty_cache()
+        case += 1
+    _log(f"fuzz: {case} cases passed")
