@@ -5,8 +5,12 @@ sequences with overlapping or gapped ranges), lengths from one of four mixes (ma
 log-normal with a heavy tail; one long among many tiny) and random launch hints (waves, chunks, plan,
 dispatch order, no workspace, no range hints), runs every partition's call, the merge and the fused
 call, and checks them against the oracle's partials and their merge (which, unlike unsplit
-attention, also covers overlapping ranges).  By default a few cases run; ``BANA_FUZZ_SECONDS=<s>``
-runs cases for that long instead (``BANA_FUZZ_SEED`` picks the stream).
+attention, also covers overlapping ranges).  On one random partition it also runs, each with some
+probability: the head-split call over a random kv-head range (its rows against the oracle, every
+other row untouched), the no-allocation call (bit for bit the workspace call's result when that ran
+with a workspace, else against the oracle; a plan beyond the static scratch must be refused), and
+the block migration of that partition (bit for bit the oracle's copy).  By default a few cases run;
+``BANA_FUZZ_SECONDS=<s>`` runs cases for that long instead (``BANA_FUZZ_SEED`` picks the stream).
 """
 
 import math
@@ -18,10 +22,10 @@ import pytest
 import torch
 
 import oracle
-from paper_2510_13223_amd import workloads as W
+from paper_2510_13223_amd import bana, workloads as W
 from paper_2510_13223_amd.runner import DeviceWorkload
 
-from test_gpu_parity import _check_lse, _check_out, _log
+from test_gpu_parity import _check_lse, _check_out, _log, _migrate_and_check
 
 pytestmark = pytest.mark.gpu
 
@@ -64,7 +68,49 @@ def _case(seed, case):
     return w, kw, f"fuzz {seed}:{case} kind={kind} B={B} Hq={Hq} Hkv={Hkv} parts={n_parts} maxL={max(lens)} {kw}"
 
 
-def _check(w, kw):
+def _extras(w, kw, dw, ro, rl, rng):
+    B, Hq, Hkv = w.batch, w.num_q_heads, w.num_kv_heads
+    G = Hq // Hkv
+    p = int(rng.integers(0, w.n_parts))
+    if Hkv > 1 and rng.random() < 0.5:
+        g0 = int(rng.integers(0, Hkv))
+        g1 = int(rng.integers(g0 + 1, Hkv + 1))
+        sub = bana.head_range_dims(dw.dims[p], g0, g1)
+        ws = torch.empty(max(256, bana.bana_decode_attn_workspace_bytes(sub)), dtype=torch.uint8, device="cuda")
+        o = torch.full((B, Hq, 128), float("nan"), device="cuda")
+        l = torch.full((B, Hq), float("nan"), device="cuda")
+        bana.bana_decode_attn_heads(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin[p],
+                                    dw.kv_end[p], g0, g1, o, l, workspace=ws, dims=dw.dims[p])
+        o, l = o.cpu().numpy(), l.cpu().numpy()
+        hs = slice(g0 * G, g1 * G)
+        fin = np.isfinite(rl[p][:, hs])
+        _check_out(o[:, hs][fin], ro[p][:, hs][fin], "head range out")
+        assert np.all(o[:, hs][~fin] == 0.0)
+        _check_lse(l[:, hs], rl[p][:, hs], "head range lse")
+        assert np.all(np.isnan(o[:, :g0 * G])) and np.all(np.isnan(o[:, g1 * G:]))
+    if rng.random() < 0.5:
+        o = torch.full((B, Hq, 128), float("nan"), device="cuda")
+        l = torch.full((B, Hq), float("nan"), device="cuda")
+        try:
+            bana.bana_decode_attn_partial_noalloc(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens,
+                                                  dw.kv_begin[p], dw.kv_end[p], o, l, dims=dw.dims[p])
+        except bana.BanaError as e:
+            assert e.status == bana.BANA_ERR_UNSUPPORTED
+            assert bana.bana_decode_attn_workspace_bytes(dw.dims[p]) > bana.STATIC_SCRATCH_BYTES
+        else:
+            torch.cuda.synchronize()
+            if kw["use_workspace"]:
+                assert torch.equal(o.view(torch.int32), dw.out_partials[p].view(torch.int32))
+                assert torch.equal(l.view(torch.int32), dw.lses[p].view(torch.int32))
+            else:
+                on, ln = o.cpu().numpy(), l.cpu().numpy()
+                _check_out(on[np.isfinite(rl[p])], ro[p][np.isfinite(rl[p])], "noalloc out_partial")
+                _check_lse(ln, rl[p], "noalloc lse")
+    if rng.random() < 0.3:
+        _migrate_and_check(w, p, seed=int(rng.integers(0, 1 << 30)), hint=bool(rng.integers(0, 2)))
+
+
+def _check(w, kw, extras_rng=None):
     dw = DeviceWorkload(w, **kw)
     op, lp, out, lse_out = dw.results()
     ro, rl = oracle.workload_partials(w)
@@ -80,6 +126,8 @@ def _check(w, kw):
     fo, fl = dw.fused_results()
     _check_out(fo[fin], mo[fin], "fused out")
     _check_lse(fl, ml, "fused lse")
+    if extras_rng is not None:
+        _extras(w, kw, dw, ro, rl, extras_rng)
 
 
 def test_random_shape_fuzz():
@@ -90,7 +138,7 @@ def test_random_shape_fuzz():
     while case < 16 or time.time() < t_end:
         w, kw, tag = _case(seed, case)
         _log(tag)
-        _check(w, kw)
+        _check(w, kw, np.random.default_rng(555000 + seed * 100000 + case))
         torch.cuda.empty_cache()
         case += 1
     _log(f"fuzz: {case} cases passed")
