@@ -8,8 +8,9 @@ call, and checks them against the oracle's partials and their merge (which, unli
 attention, also covers overlapping ranges).  On one random partition it also runs, each with some
 probability: the head-split call over a random kv-head range (its rows against the oracle, every
 other row untouched), the no-allocation call (bit for bit the workspace call's result when that ran
-with a workspace, else against the oracle; a plan beyond the static scratch must be refused), and
-the block migration of that partition (bit for bit the oracle's copy).  By default a few cases run;
+with a workspace, else against the oracle; a plan beyond the static scratch must be refused), the
+block migration of that partition (bit for bit the oracle's copy), and the fused call with 0-8
+random side copies (bit for bit the fused call with the chunked launch; every copy byte for byte).  By default a few cases run;
 ``BANA_FUZZ_SECONDS=<s>`` runs cases for that long instead (``BANA_FUZZ_SEED`` picks the stream).
 """
 
@@ -108,6 +109,48 @@ def _extras(w, kw, dw, ro, rl, rng):
                 _check_lse(ln, rl[p], "noalloc lse")
     if rng.random() < 0.3:
         _migrate_and_check(w, p, seed=int(rng.integers(0, 1 << 30)), hint=bool(rng.integers(0, 2)))
+    if rng.random() < 0.3:
+        _fused_copies(w, kw, dw, rng)
+
+
+def _fused_copies(w, kw, dw, rng):
+    """The fused call with 0-8 random side copies equals the fused call with the chunked launch bit for
+    bit, and every copy arrives byte for byte."""
+    B, Hq = w.batch, w.num_q_heads
+    fd = bana.bana_dims.from_buffer_copy(dw.fused_dims)
+    fd.plan_hint = 1
+    ws = None
+    if kw["use_workspace"]:
+        ws = torch.empty(max(256, bana.bana_decode_attn_workspace_bytes(fd)), dtype=torch.uint8, device="cuda")
+    ref_o = torch.empty((B, Hq, 128), device="cuda")
+    ref_l = torch.empty((B, Hq), device="cuda")
+    bana.bana_decode_attn_fused(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin, dw.kv_end,
+                                ref_o, ref_l, workspace=ws, dims=fd)
+    g = torch.Generator().manual_seed(int(rng.integers(0, 1 << 30)))
+    copies, checks = [], []
+    for _ in range(int(rng.integers(0, 9))):
+        n = 4 * int(rng.integers(0, 1 << 17))  # int32 words: 0 to 2 MiB, a multiple of 16 bytes
+        kind = int(rng.integers(0, 3))
+        src = torch.randint(-2**31, 2**31 - 1, (n,), dtype=torch.int32, generator=g)
+        if n == 0:
+            src, dst = src.cuda(), torch.empty(0, dtype=torch.int32, device="cuda")
+        elif kind == 0:  # pinned host -> device
+            src, dst = src.pin_memory(), torch.zeros(n, dtype=torch.int32, device="cuda")
+        elif kind == 1:  # device -> pinned host
+            src, dst = src.cuda(), torch.zeros(n, dtype=torch.int32).pin_memory()
+        else:  # device -> device
+            src, dst = src.cuda(), torch.zeros(n, dtype=torch.int32, device="cuda")
+        copies.append((dst, src))
+        checks.append((dst, src))
+    o = torch.full((B, Hq, 128), float("nan"), device="cuda")
+    l = torch.full((B, Hq), float("nan"), device="cuda")
+    bana.bana_decode_attn_fused_copies(dw.q, dw.k_cache, dw.v_cache, dw.block_table, dw.seq_lens, dw.kv_begin,
+                                       dw.kv_end, o, l, copies=copies, workspace=ws, dims=dw.fused_dims)
+    torch.cuda.synchronize()
+    assert torch.equal(o.view(torch.int32), ref_o.view(torch.int32))
+    assert torch.equal(l.view(torch.int32), ref_l.view(torch.int32))
+    for dst, src in checks:
+        assert torch.equal(dst.cpu(), src.cpu())
 
 
 def _check(w, kw, extras_rng=None):
