@@ -33,6 +33,8 @@ def summarize(t: np.ndarray) -> Dict[str, float]:
     used = t[:, 0] != UNSET
     t = t[used]
     n = len(t)
+    if n == 0:
+        raise ValueError("no wavefront recorded an entry")
     t0 = t[:, 0].min()
     rel = lambda col: (t[:, col] - t0).astype(np.float64) * TICK_US
     entry, ready, exit_ = rel(0), rel(1), rel(3)
@@ -42,7 +44,7 @@ def summarize(t: np.ndarray) -> Dict[str, float]:
     q = lambda x, p: float(np.nanpercentile(x, p)) if np.isfinite(x).any() else float("nan")
     s = {
         "waves": n,
-        "span_us": float(exit_[done].max()),
+        "span_us": float(exit_[done].max()) if done.any() else float("nan"),
         "entry_spread_us": float(entry.max()),
         "ready_after_entry_p50_us": q(ready - entry, 50),
         "first_block_after_entry_p10_us": q(first - entry, 10),
@@ -127,8 +129,8 @@ def main(argv=None) -> None:
     args = ap.parse_args(argv)
     rows = run(args.cases, args.reps)
     if args.md:
-        cmd = "python -m paper_2510_13223_amd.timeline " + " ".join(
-            (["--reps", str(args.reps)] if args.reps != 3 else []) + args.cases)
+        cmd = "python -u -m paper_2510_13223_amd.timeline " + " ".join(
+            (["--reps", str(args.reps)] if args.reps != 3 else []) + ["--md", args.md] + args.cases)
         with open(args.md, "w") as f:
             f.write(markdown(rows, cmd))
 

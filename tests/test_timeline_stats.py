@@ -25,3 +25,14 @@ def test_summarize_known_table():
     # quarters in slot order: two slots each
     assert abs(s["q0_exit_p50_us"] - 10.5) < 1e-9 and abs(s["q3_exit_p50_us"] - 16.5) < 1e-9
     assert abs(s["q1_first_block_p50_us"] - 4.0) < 1e-9  # slot 2 only (slot 3 has no reading)
+
+
+def test_summarize_without_exits_or_entries():
+    import pytest
+
+    t = np.full((4, 4), timeline.UNSET, dtype=np.uint64)
+    with pytest.raises(ValueError):
+        timeline.summarize(t)
+    t[0] = (100, 110, timeline.UNSET, timeline.UNSET)  # entered and scheduled, never finished
+    s = timeline.summarize(t)
+    assert s["waves"] == 1 and np.isnan(s["span_us"]) and np.isnan(s["exit_p50_us"])
